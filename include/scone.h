@@ -1,0 +1,168 @@
+/*
+ * scone.h: C ABI of the MI355X f-gram embedding library (libscone.so).
+ *
+ * The library implements the inference branch of the SCONE embedding
+ * (Algorithm 1 of "Scaling Embedding Layers in Language Models"): for each
+ * token it finds the longest f-gram that ends at that token, maps it to a row
+ * id, and copies that row of a precomputed embedding table; when no f-gram
+ * matches it copies the token's own row.  The f-gram layer is a key-value
+ * store from f-grams to rows (Section 2: a dense matrix plus a hash
+ * dictionary to row indices), and the rows live either in HBM or in
+ * host-pinned memory read over PCIe (the off-accelerator placement of
+ * Sections 2 and 3.2).
+ *
+ * Conventions for every call:
+ *  - Pointers are device pointers unless stated otherwise; "host-mapped"
+ *    means a device-accessible pointer to pinned host memory (see
+ *    scone_host_alloc).
+ *  - `stream` is a hipStream_t passed as void*; NULL is the default stream.
+ *    Calls run on the calling thread's current HIP device.
+ *  - Every call returns a scone_status.  Argument errors are detected on the
+ *    host before any launch and change nothing.  Errors that depend on
+ *    device data (SCONE_ETOKEN, SCONE_EROW) cannot be seen by the host
+ *    without a sync: asynchronous calls raise them in the device's error
+ *    word and report them through scone_check().  After such an error the
+ *    contents of the outputs are unspecified.
+ *  - No call allocates device memory except scone_build_fgram_table and
+ *    scone_host_alloc (and a 4-byte error word per device on first use).
+ *  - All buffers are owned by the caller except the table handle, which the
+ *    library owns until scone_table_destroy.
+ */
+#ifndef SCONE_H
+#define SCONE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct scone_table scone_table_t;
+
+enum scone_status {
+    SCONE_OK = 0,
+    SCONE_EINVAL = 1,  /* bad argument: null pointer, negative size, bad window ... */
+    SCONE_ELEN = 2,    /* an f-gram length outside [2, max_len] */
+    SCONE_EID = 3,     /* a negative f-gram id */
+    SCONE_EDUP = 4,    /* the same f-gram appears twice in the build input */
+    SCONE_EFULL = 5,   /* hash table has no free slot (cannot happen for max_load <= 0.9) */
+    SCONE_ENOMEM = 6,  /* device or pinned host allocation failed */
+    SCONE_EHIP = 7,    /* a HIP runtime call failed */
+    SCONE_ETOKEN = 8,  /* a token outside [0, SCONE_TOKEN_LIMIT) */
+    SCONE_EROW = 9     /* a row id outside [0, n_rows) */
+};
+
+enum scone_placement {
+    SCONE_PLACE_HBM = 0,   /* `rows` is device memory */
+    SCONE_PLACE_HOST = 1   /* `rows` is host-mapped pinned memory, read over PCIe */
+};
+
+#define SCONE_MAX_FGRAM_LEN 7     /* longest f-gram a table can hold */
+#define SCONE_TOKEN_LIMIT 65536   /* tokens are packed as 16-bit fields */
+
+/*
+ * Build the f-gram dictionary (the key-value store F of Algorithm 1, whose
+ * keys are the set V_fgram of Section 3; F is precomputed before serving,
+ * Section 3.2).
+ *
+ *  fgrams   [n, max_len] int32 row-major; row k holds f-gram k's tokens,
+ *           oldest first, in its first lengths[k] entries (the rest is
+ *           ignored and may hold anything).
+ *  lengths  [n] int32, each in [2, max_len]   (else SCONE_ELEN; V_fgram is a
+ *           subset of V^[2,K]).
+ *  ids      [n] int32 row ids, each >= 0      (else SCONE_EID).  Ids are not
+ *           checked against a row count here; scone_gather checks them.
+ *  n        number of f-grams, >= 0 (0 builds an empty set).
+ *  max_len  K, in [2, SCONE_MAX_FGRAM_LEN].  K <= 5 uses 16-byte slots,
+ *           K = 6 or 7 uses 32-byte slots.
+ *  max_load target load factor in (0, 0.9]; the slot count is the smallest
+ *           power of two >= max(64, n / max_load).
+ *  stream   stream on which the inputs are ready.
+ *  out      receives the new table handle (host pointer to a handle).
+ *
+ * Tokens must lie in [0, SCONE_TOKEN_LIMIT) (else SCONE_ETOKEN).  A repeated
+ * f-gram (same length, same tokens) gives SCONE_EDUP: V_fgram is a set.
+ * The call is synchronous: it waits on `stream` and returns the first data
+ * error found.  On any error *out is NULL and nothing stays allocated.  The
+ * caller may free its inputs as soon as the call returns.
+ */
+int scone_build_fgram_table(const int32_t* fgrams, const int32_t* lengths,
+                            const int32_t* ids, int64_t n, int32_t max_len,
+                            double max_load, void* stream, scone_table_t** out);
+
+/*
+ * Longest-suffix lookup (Algorithm 1, the choice of j): for every b < B and
+ * t < T, fgram_ids[b,t] is the id of the longest f-gram
+ * (X[b,t-n+1], ..., X[b,t]) with 2 <= n <= min(max_n, t+1) that is in the
+ * table, and match_len[b,t] = n; when there is none, fgram_ids[b,t] =
+ * X[b,t] (the token's own row) and match_len[b,t] = 1.  Windows never reach
+ * before t = 0 of their own row.  Every length is tested on its own, so the
+ * f-gram set need not contain the suffixes of its members.
+ *
+ *  token_ids  [B, T] int32 row-major, each in [0, SCONE_TOKEN_LIMIT)
+ *             (else SCONE_ETOKEN via scone_check).
+ *  max_n      >= 1; values above the table's max_len behave as max_len;
+ *             1 gives the identity.
+ *  fgram_ids  [B, T] int32 output.
+ *  match_len  [B, T] int8 output, or NULL.
+ *
+ * Asynchronous on `stream`; the table is read-only, so concurrent lookups on
+ * one table are safe.  B * T = 0 launches nothing.
+ */
+int scone_lookup(const scone_table_t* table, const int32_t* token_ids, int64_t B,
+                 int64_t T, int32_t max_n, int32_t* fgram_ids, int8_t* match_len,
+                 void* stream);
+
+/*
+ * Row gather (the embedding fetch; Section 1 notes it is a pure memory read):
+ * out[k, :] = rows[fgram_ids[k], :] for k < n_tok, copied as raw bytes, so
+ * any element type (fp32, bf16, ...) is reproduced bit for bit.
+ *
+ *  fgram_ids  [n_tok] int32, each in [0, n_rows) (else SCONE_EROW via
+ *             scone_check; that output row is then zero-filled).
+ *  rows       [n_rows, row_bytes] table: device memory (placement
+ *             SCONE_PLACE_HBM) or host-mapped pinned memory
+ *             (SCONE_PLACE_HOST).
+ *  row_bytes  > 0.  Rows move in 16-byte vectors when row_bytes and both
+ *             pointers allow it, otherwise in the widest unit that does.
+ *  out        [n_tok, row_bytes] device output; must not overlap `rows`.
+ *
+ * Asynchronous on `stream`.  n_tok = 0 launches nothing.
+ */
+int scone_gather(const int32_t* fgram_ids, int64_t n_tok, const void* rows,
+                 int64_t n_rows, int64_t row_bytes, void* out, int32_t placement,
+                 void* stream);
+
+/*
+ * Allocate `bytes` of pinned host memory that kernels can read over PCIe
+ * (the off-accelerator row store of Section 4.3).  *host_ptr receives the
+ * host address, *device_ptr the address to pass to scone_gather with
+ * SCONE_PLACE_HOST.  SCONE_ENOMEM on failure.  Free with scone_host_free.
+ */
+int scone_host_alloc(int64_t bytes, void** host_ptr, void** device_ptr);
+int scone_host_free(void* host_ptr);
+
+/*
+ * Wait for `stream`, then read and clear the current device's error word.
+ * Returns SCONE_OK or the lowest data-error code raised by the asynchronous
+ * calls since the last check (SCONE_ETOKEN, SCONE_EROW, SCONE_EFULL).  The
+ * word is per device, not per stream: concurrent streams share it.
+ */
+int scone_check(void* stream);
+
+/* Free a table (NULL is a no-op).  The caller must not use it afterwards and
+ * must make sure no lookup that reads it is still running. */
+void scone_table_destroy(scone_table_t* table);
+
+/* Properties of a built table; any output pointer may be NULL. */
+int scone_table_info(const scone_table_t* table, int64_t* n, int64_t* capacity,
+                     int32_t* max_len, int32_t* slot_bytes);
+
+/* A static, human-readable description of a status code. */
+const char* scone_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SCONE_H */

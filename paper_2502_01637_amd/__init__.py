@@ -1,0 +1,12 @@
+"""MI355X (gfx950) implementation of SCONE's inference-time f-gram embedding path.
+
+The C ABI (include/scone.h, built as libscone.so) holds the hash-table build,
+the longest-suffix lookup and the row gather as HIP kernels; ``scone`` is its
+Python binding.
+"""
+from . import scone
+from .scone import (SconeError, Table, HostRows, build_fgram_table, lookup, gather, check,
+                    check_ok)
+
+__all__ = ["scone", "SconeError", "Table", "HostRows", "build_fgram_table", "lookup", "gather",
+           "check", "check_ok"]

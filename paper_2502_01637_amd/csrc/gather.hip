@@ -1,0 +1,141 @@
+// Row gather: out[k, :] = rows[ids[k], :] as raw bytes.
+//
+// The embedding fetch is a pure memory copy (Section 1), so the kernel is an
+// HBM-bound streaming copy whose source rows are chosen by the ids.  The
+// output is viewed as a flat array of V-sized units (16 bytes when the row
+// width and the pointers allow).  Consecutive lanes own consecutive units, so
+// one wavefront reads 64 * 16 B = 1 KiB of one row per instruction and writes
+// the same 1 KiB of the output; each thread issues all of its U loads before
+// its U stores to keep enough bytes in flight.  Output stores are
+// non-temporal: the output is not re-read by this path, and keeping it out of
+// the caches leaves them to the table rows that repeat (frequent tokens).
+// The same kernel reads a host-mapped pinned table over PCIe when the rows
+// live off the accelerator.
+#include "scone_internal.h"
+
+namespace scone {
+namespace {
+
+constexpr int kGatherThreads = 256;
+
+template <typename V, int U, bool kPow2>
+__global__ __launch_bounds__(kGatherThreads) void k_gather(
+    const int32_t* __restrict__ ids, int64_t total, const V* __restrict__ rows, int64_t n_rows,
+    int64_t upr, int shift, V* __restrict__ out, unsigned* __restrict__ err) {
+    const int64_t base = (int64_t)blockIdx.x * (kGatherThreads * U) + threadIdx.x;
+    V v[U];
+    bool ok[U];
+    if (base + (int64_t)(U - 1) * kGatherThreads < total) {
+        // Whole block in range: every load is unconditional so that all U
+        // id loads, then all U row loads, are in flight together.  A bad id
+        // reads row 0 instead and its unit is zeroed afterwards.
+        int64_t id[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = base + (int64_t)u * kGatherThreads;
+            id[u] = ids[kPow2 ? (i >> shift) : (i / upr)];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = base + (int64_t)u * kGatherThreads;
+            const int64_t r = kPow2 ? (i >> shift) : (i / upr);
+            const int64_t c = i - r * upr;
+            ok[u] = (id[u] >= 0) & (id[u] < n_rows);
+            const int64_t src = ok[u] ? id[u] : 0;
+            v[u] = rows[(kPow2 ? (src << shift) : src * upr) + c];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (!ok[u]) v[u] = V{};
+            __builtin_nontemporal_store(v[u], out + base + (int64_t)u * kGatherThreads);
+        }
+    } else {
+        // Ragged last block.
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = base + (int64_t)u * kGatherThreads;
+            ok[u] = true;
+            if (i < total) {
+                const int64_t r = kPow2 ? (i >> shift) : (i / upr);
+                const int64_t c = i - r * upr;
+                const int64_t id = ids[r];
+                ok[u] = (id >= 0) & (id < n_rows);
+                v[u] = ok[u] ? rows[id * upr + c] : V{};
+                __builtin_nontemporal_store(v[u], out + i);
+            }
+        }
+    }
+    bool bad = false;
+#pragma unroll
+    for (int u = 0; u < U; ++u) bad |= !ok[u];
+    if (bad) atomicOr(err, err_bit(SCONE_EROW));
+}
+
+// Every id is out of range when the table has no rows: zero the output.
+template <typename V>
+__global__ __launch_bounds__(kGatherThreads) void k_zero(int64_t total, V* __restrict__ out,
+                                                         unsigned* __restrict__ err) {
+    const int64_t i = (int64_t)blockIdx.x * kGatherThreads + threadIdx.x;
+    if (i < total) out[i] = V{};
+    if (i == 0) atomicOr(err, err_bit(SCONE_EROW));
+}
+
+template <typename V, int U>
+hipError_t launch_gather(const int32_t* ids, int64_t n_tok, const void* rows, int64_t n_rows,
+                         int64_t row_bytes, void* out, unsigned* err, hipStream_t st) {
+    const int64_t upr = row_bytes / (int64_t)sizeof(V);
+    const int64_t total = n_tok * upr;
+    const int64_t grid = (total + kGatherThreads * U - 1) / (kGatherThreads * U);
+    if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    if (n_rows == 0) {
+        const int64_t zgrid = (total + kGatherThreads - 1) / kGatherThreads;
+        if (zgrid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+        hipLaunchKernelGGL(k_zero<V>, dim3((unsigned)zgrid), dim3(kGatherThreads), 0, st, total,
+                           static_cast<V*>(out), err);
+        return hipGetLastError();
+    }
+    const bool pow2 = (upr & (upr - 1)) == 0;
+    int shift = 0;
+    while (((int64_t)1 << shift) < upr) ++shift;
+    if (pow2)
+        hipLaunchKernelGGL((k_gather<V, U, true>), dim3((unsigned)grid), dim3(kGatherThreads), 0,
+                           st, ids, total, static_cast<const V*>(rows), n_rows, upr, shift,
+                           static_cast<V*>(out), err);
+    else
+        hipLaunchKernelGGL((k_gather<V, U, false>), dim3((unsigned)grid), dim3(kGatherThreads),
+                           0, st, ids, total, static_cast<const V*>(rows), n_rows, upr, shift,
+                           static_cast<V*>(out), err);
+    return hipGetLastError();
+}
+
+}  // namespace
+}  // namespace scone
+
+extern "C" int scone_gather(const int32_t* fgram_ids, int64_t n_tok, const void* rows,
+                            int64_t n_rows, int64_t row_bytes, void* out, int32_t placement,
+                            void* stream) {
+    using namespace scone;
+    if (n_tok < 0 || n_rows < 0 || row_bytes <= 0) return SCONE_EINVAL;
+    if (placement != SCONE_PLACE_HBM && placement != SCONE_PLACE_HOST) return SCONE_EINVAL;
+    if (n_tok > ((int64_t)1 << 62) / row_bytes) return SCONE_EINVAL;
+    if (n_tok == 0) return SCONE_OK;
+    if (!fgram_ids || !out || (!rows && n_rows > 0)) return SCONE_EINVAL;
+    unsigned* err = device_error_word();
+    if (!err) return SCONE_EHIP;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    // Widest unit that divides the row width and both base addresses.
+    const uintptr_t align = (uintptr_t)rows | (uintptr_t)out | (uintptr_t)row_bytes;
+    hipError_t e;
+    if ((align & 15) == 0)
+        e = launch_gather<u32x4, 4>(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err, st);
+    else if ((align & 7) == 0)
+        e = launch_gather<u32x2, 4>(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err, st);
+    else if ((align & 3) == 0)
+        e = launch_gather<uint32_t, 4>(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err, st);
+    else if ((align & 1) == 0)
+        e = launch_gather<uint16_t, 4>(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err, st);
+    else
+        e = launch_gather<uint8_t, 4>(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err, st);
+    if (e == hipErrorInvalidConfiguration) return SCONE_EINVAL;
+    return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
+}

@@ -1,0 +1,165 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "scone.h"
+
+namespace scone {
+
+// ---------------------------------------------------------------- errors ---
+
+__host__ __device__ constexpr unsigned err_bit(int code) { return 1u << code; }
+
+// Lowest status code whose bit is set in `word` (SCONE_OK for 0).
+int code_from_bits(unsigned word);
+
+// The current device's 4-byte error word (allocated on first use), or null if
+// the allocation failed.
+unsigned* device_error_word();
+
+#define SCONE_HIP_TRY(expr)                                \
+    do {                                                   \
+        if ((expr) != hipSuccess) return SCONE_EHIP;       \
+    } while (0)
+
+// ---------------------------------------------------------- f-gram keys ----
+// An f-gram of n <= 7 tokens, each < 2^16, is one bit string:
+//   bits [0, 4)              the length n
+//   bits [4 + 16k, 20 + 16k) token k, oldest first
+// held in two 64-bit words.  n <= 5 uses at most 84 bits, so its second word
+// fits 32 bits and the key fits a 16-byte slot next to a 32-bit id.  A valid
+// key never has a zero first word (n >= 2), so zero marks an empty slot.
+
+constexpr int kTokenBits = 16;
+constexpr int kMaxLenSlot16 = 5;
+
+struct Key {
+    uint64_t w0;
+    uint64_t w1;
+};
+
+// Pack tokens tok[0..n) (n <= 7); the caller guarantees every token is in
+// [0, 2^16).
+template <typename Tok>
+__device__ __forceinline__ Key pack_key(const Tok* tok, int n) {
+    Key k{(uint64_t)n, 0};
+#pragma unroll
+    for (int i = 0; i < SCONE_MAX_FGRAM_LEN; ++i) {
+        if (i < n) {
+            const uint64_t v = (uint64_t)(uint32_t)tok[i];
+            const int p = 4 + kTokenBits * i;
+            if (p < 64) {
+                k.w0 |= v << p;
+                if (p + kTokenBits > 64) k.w1 |= v >> (64 - p);
+            } else {
+                k.w1 |= v << (p - 64);
+            }
+        }
+    }
+    return k;
+}
+
+// MurmurHash3's 64-bit finalizer (Appleby), applied to the two key words.
+__device__ __forceinline__ uint64_t fmix64(uint64_t x) {
+    x ^= x >> 33;
+    x *= 0xff51afd7ed558ccdULL;
+    x ^= x >> 33;
+    x *= 0xc4ceb9fe1a85ec53ULL;
+    x ^= x >> 33;
+    return x;
+}
+
+__device__ __forceinline__ uint64_t hash_key(const Key& k) {
+    return fmix64(k.w0 ^ (k.w1 * 0x9E3779B97F4A7C15ULL));
+}
+
+// ---------------------------------------------------------------- slots ----
+
+struct alignas(16) Slot16 {
+    uint64_t w0;
+    uint32_t w1;
+    int32_t id;
+};
+
+struct alignas(32) Slot32 {
+    uint64_t w0;
+    uint64_t w1;
+    int32_t id;
+    int32_t pad[3];
+};
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <int SB>
+struct SlotOps;
+
+template <>
+struct SlotOps<16> {
+    using Slot = Slot16;
+    // One 16-byte load returns the whole slot.
+    __device__ __forceinline__ static void read(const Slot16* base, uint64_t s, uint64_t& w0,
+                                                uint64_t& w1, int32_t& id) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(base + s);
+        w0 = (uint64_t)v.x | ((uint64_t)v.y << 32);
+        w1 = v.z;
+        id = (int32_t)v.w;
+    }
+    __device__ __forceinline__ static void write_rest(Slot16* base, uint64_t s, const Key& k,
+                                                      int32_t id) {
+        base[s].w1 = (uint32_t)k.w1;
+        base[s].id = id;
+    }
+};
+
+template <>
+struct SlotOps<32> {
+    using Slot = Slot32;
+    __device__ __forceinline__ static void read(const Slot32* base, uint64_t s, uint64_t& w0,
+                                                uint64_t& w1, int32_t& id) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(base + s);
+        const uint32_t c = reinterpret_cast<const uint32_t*>(base + s)[4];
+        w0 = (uint64_t)a.x | ((uint64_t)a.y << 32);
+        w1 = (uint64_t)a.z | ((uint64_t)a.w << 32);
+        id = (int32_t)c;
+    }
+    __device__ __forceinline__ static void write_rest(Slot32* base, uint64_t s, const Key& k,
+                                                      int32_t id) {
+        base[s].w1 = k.w1;
+        base[s].id = id;
+    }
+};
+
+// Linear probe from the key's home slot.  Returns true and the id on a hit;
+// false when an empty slot is reached first.  Bounded by the slot count.
+template <int SB>
+__device__ __forceinline__ bool probe(const typename SlotOps<SB>::Slot* slots, uint64_t mask,
+                                      const Key& k, int32_t& id_out) {
+    uint64_t s = hash_key(k) & mask;
+    for (uint64_t step = 0; step <= mask; ++step) {
+        uint64_t w0, w1;
+        int32_t id;
+        SlotOps<SB>::read(slots, s, w0, w1, id);
+        if (w0 == k.w0 && w1 == k.w1) {
+            id_out = id;
+            return true;
+        }
+        if (w0 == 0) return false;
+        s = (s + 1) & mask;
+    }
+    return false;
+}
+
+}  // namespace scone
+
+// The opaque table handle.
+struct scone_table {
+    int device;
+    int32_t max_len;    // longest f-gram the table can hold (K)
+    int32_t slot_bytes; // 16 or 32
+    int64_t n;          // f-grams stored
+    int64_t capacity;   // slots, a power of two
+    void* slots;        // device memory, capacity * slot_bytes
+};

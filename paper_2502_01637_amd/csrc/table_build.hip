@@ -1,0 +1,206 @@
+// Building the f-gram dictionary: an open-addressing hash table in HBM.
+//
+// The paper stores the f-gram layer as a dense row matrix plus a hash
+// dictionary from f-grams to row indices (Section 2), built before serving
+// (Section 3.2).  Here the dictionary is a power-of-two array of slots with
+// linear probing.  Insertion claims the first empty slot on the key's probe
+// path with a 64-bit compare-and-swap on the slot's first key word, then
+// writes the rest of the key and the id; it never compares keys, so slot
+// placement under concurrency does not matter.  A second pass re-probes every
+// input key: the first slot holding that key must be the one its own thread
+// claimed, otherwise the key was inserted twice (a duplicate f-gram).
+#include <algorithm>
+#include <cmath>
+
+#include "scone_internal.h"
+
+namespace scone {
+namespace {
+
+constexpr int kBuildThreads = 256;
+
+template <typename Tok>
+__device__ __forceinline__ bool tokens_in_range(const Tok* tok, int n) {
+    bool ok = true;
+    for (int i = 0; i < n; ++i) ok &= (tok[i] >= 0) & (tok[i] < SCONE_TOKEN_LIMIT);
+    return ok;
+}
+
+template <int SB>
+__global__ __launch_bounds__(kBuildThreads) void k_insert(
+    const int32_t* __restrict__ fgrams, const int32_t* __restrict__ lengths,
+    const int32_t* __restrict__ ids, int64_t n, int max_len,
+    typename SlotOps<SB>::Slot* __restrict__ slots, uint64_t mask,
+    int64_t* __restrict__ slot_of, unsigned* __restrict__ status) {
+    const int64_t k = (int64_t)blockIdx.x * kBuildThreads + threadIdx.x;
+    if (k >= n) return;
+    slot_of[k] = -1;
+    const int len = lengths[k];
+    const int32_t id = ids[k];
+    if (len < 2 || len > max_len) {
+        atomicOr(status, err_bit(SCONE_ELEN));
+        return;
+    }
+    if (id < 0) {
+        atomicOr(status, err_bit(SCONE_EID));
+        return;
+    }
+    const int32_t* tok = fgrams + k * (int64_t)max_len;
+    if (!tokens_in_range(tok, len)) {
+        atomicOr(status, err_bit(SCONE_ETOKEN));
+        return;
+    }
+    const Key key = pack_key(tok, len);
+    uint64_t s = hash_key(key) & mask;
+    for (uint64_t step = 0; step <= mask; ++step) {
+        unsigned long long* w0 = reinterpret_cast<unsigned long long*>(&slots[s].w0);
+        if (atomicCAS(w0, 0ull, (unsigned long long)key.w0) == 0ull) {
+            SlotOps<SB>::write_rest(slots, s, key, id);
+            slot_of[k] = (int64_t)s;
+            return;
+        }
+        s = (s + 1) & mask;
+    }
+    atomicOr(status, err_bit(SCONE_EFULL));
+}
+
+template <int SB>
+__global__ __launch_bounds__(kBuildThreads) void k_verify(
+    const int32_t* __restrict__ fgrams, const int32_t* __restrict__ lengths, int64_t n,
+    int max_len, const typename SlotOps<SB>::Slot* __restrict__ slots, uint64_t mask,
+    const int64_t* __restrict__ slot_of, unsigned* __restrict__ status) {
+    const int64_t k = (int64_t)blockIdx.x * kBuildThreads + threadIdx.x;
+    if (k >= n) return;
+    const int64_t mine = slot_of[k];
+    if (mine < 0) return;  // rejected or not placed: already reported
+    const Key key = pack_key(fgrams + k * (int64_t)max_len, lengths[k]);
+    uint64_t s = hash_key(key) & mask;
+    for (uint64_t step = 0; step <= mask; ++step) {
+        uint64_t w0, w1;
+        int32_t id;
+        SlotOps<SB>::read(slots, s, w0, w1, id);
+        if (w0 == key.w0 && w1 == key.w1) {
+            if ((int64_t)s != mine) atomicOr(status, err_bit(SCONE_EDUP));
+            return;
+        }
+        if (w0 == 0) break;
+        s = (s + 1) & mask;
+    }
+    // Its own slot lies on its probe path, so reaching here is a broken table.
+    atomicOr(status, err_bit(SCONE_EFULL));
+}
+
+template <int SB>
+hipError_t launch_build(const int32_t* fgrams, const int32_t* lengths, const int32_t* ids,
+                        int64_t n, int max_len, void* slots, uint64_t mask, int64_t* slot_of,
+                        unsigned* status, hipStream_t st) {
+    using Slot = typename SlotOps<SB>::Slot;
+    const unsigned grid = (unsigned)((n + kBuildThreads - 1) / kBuildThreads);
+    hipLaunchKernelGGL(k_insert<SB>, dim3(grid), dim3(kBuildThreads), 0, st, fgrams, lengths,
+                       ids, n, max_len, static_cast<Slot*>(slots), mask, slot_of, status);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_verify<SB>, dim3(grid), dim3(kBuildThreads), 0, st, fgrams, lengths, n,
+                       max_len, static_cast<const Slot*>(slots), mask, slot_of, status);
+    return hipGetLastError();
+}
+
+}  // namespace
+}  // namespace scone
+
+extern "C" int scone_build_fgram_table(const int32_t* fgrams, const int32_t* lengths,
+                                       const int32_t* ids, int64_t n, int32_t max_len,
+                                       double max_load, void* stream, scone_table_t** out) {
+    using namespace scone;
+    if (!out) return SCONE_EINVAL;
+    *out = nullptr;
+    if (n < 0 || max_len < 2 || max_len > SCONE_MAX_FGRAM_LEN) return SCONE_EINVAL;
+    if (!(max_load > 0.0 && max_load <= 0.9)) return SCONE_EINVAL;
+    if (n > 0 && (!fgrams || !lengths || !ids)) return SCONE_EINVAL;
+    // Slot count: smallest power of two >= max(64, n / max_load), at most 2^40.
+    const double want = std::max(64.0, std::ceil((double)n / max_load));
+    if (want > (double)(1ull << 40)) return SCONE_EINVAL;
+    uint64_t cap = 64;
+    while ((double)cap < want) cap <<= 1;
+    const int slot_bytes = max_len <= kMaxLenSlot16 ? 16 : 32;
+    const unsigned grid = (unsigned)((n + 255) / 256);
+    if ((uint64_t)grid > 0x7fffffffull) return SCONE_EINVAL;
+
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    int dev = 0;
+    SCONE_HIP_TRY(hipGetDevice(&dev));
+
+    void* slots = nullptr;
+    unsigned* status = nullptr;
+    int64_t* slot_of = nullptr;
+    int rc = SCONE_OK;
+    unsigned hstatus = 0;
+    if (hipMalloc(&slots, cap * (uint64_t)slot_bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return SCONE_ENOMEM;
+    }
+    if (hipMalloc(&status, sizeof(unsigned)) != hipSuccess ||
+        (n > 0 && hipMalloc(&slot_of, sizeof(int64_t) * (size_t)n) != hipSuccess)) {
+        (void)hipGetLastError();
+        rc = SCONE_ENOMEM;
+        goto fail;
+    }
+    if (hipMemsetAsync(slots, 0, cap * (uint64_t)slot_bytes, st) != hipSuccess ||
+        hipMemsetAsync(status, 0, sizeof(unsigned), st) != hipSuccess) {
+        rc = SCONE_EHIP;
+        goto fail;
+    }
+    if (n > 0) {
+        const hipError_t e =
+            slot_bytes == 16
+                ? launch_build<16>(fgrams, lengths, ids, n, max_len, slots, cap - 1, slot_of,
+                                   status, st)
+                : launch_build<32>(fgrams, lengths, ids, n, max_len, slots, cap - 1, slot_of,
+                                   status, st);
+        if (e != hipSuccess) {
+            rc = SCONE_EHIP;
+            goto fail;
+        }
+    }
+    if (hipMemcpyAsync(&hstatus, status, sizeof(unsigned), hipMemcpyDeviceToHost, st) !=
+            hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess) {
+        rc = SCONE_EHIP;
+        goto fail;
+    }
+    if (hstatus) {
+        // Report argument-like data errors before structural ones.
+        const int order[] = {SCONE_ELEN, SCONE_EID, SCONE_ETOKEN, SCONE_EDUP, SCONE_EFULL};
+        rc = SCONE_EFULL;
+        for (int c : order)
+            if (hstatus & err_bit(c)) {
+                rc = c;
+                break;
+            }
+        goto fail;
+    }
+    (void)hipFree(status);
+    if (slot_of) (void)hipFree(slot_of);
+    {
+        scone_table* t = new (std::nothrow) scone_table();
+        if (!t) {
+            (void)hipFree(slots);
+            return SCONE_ENOMEM;
+        }
+        t->device = dev;
+        t->max_len = max_len;
+        t->slot_bytes = slot_bytes;
+        t->n = n;
+        t->capacity = (int64_t)cap;
+        t->slots = slots;
+        *out = t;
+    }
+    return SCONE_OK;
+
+fail:
+    (void)hipStreamSynchronize(st);
+    if (slots) (void)hipFree(slots);
+    if (status) (void)hipFree(status);
+    if (slot_of) (void)hipFree(slot_of);
+    return rc;
+}

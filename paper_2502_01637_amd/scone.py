@@ -1,0 +1,250 @@
+"""Python binding of libscone.so (argument marshalling only).
+
+Every function here checks dtypes, devices and shapes, then passes raw
+pointers and sizes to the C ABI declared in ``include/scone.h``; all of the
+lookup and gather work runs in the library's HIP kernels.  PyTorch supplies
+device memory and the current stream.  When the library is missing or cannot
+be loaded, every call raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Optional, Tuple
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libscone.so")
+
+OK, EINVAL, ELEN, EID, EDUP, EFULL, ENOMEM, EHIP, ETOKEN, EROW = range(10)
+PLACE_HBM, PLACE_HOST = 0, 1
+MAX_FGRAM_LEN = 7
+TOKEN_LIMIT = 65536
+
+_lib = None
+_lock = threading.Lock()
+
+
+class SconeError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        msg = lib().scone_strerror(code).decode() if _lib is not None else str(code)
+        super().__init__(f"{what}: {msg} (status {code})")
+        self.code = code
+
+
+def _declare(L):
+    P, I64, I32, I = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int
+    L.scone_build_fgram_table.argtypes = [P, P, P, I64, I32, ctypes.c_double, P,
+                                          ctypes.POINTER(P)]
+    L.scone_build_fgram_table.restype = I
+    L.scone_lookup.argtypes = [P, P, I64, I64, I32, P, P, P]
+    L.scone_lookup.restype = I
+    L.scone_gather.argtypes = [P, I64, P, I64, I64, P, I32, P]
+    L.scone_gather.restype = I
+    L.scone_host_alloc.argtypes = [I64, ctypes.POINTER(P), ctypes.POINTER(P)]
+    L.scone_host_alloc.restype = I
+    L.scone_host_free.argtypes = [P]
+    L.scone_host_free.restype = I
+    L.scone_check.argtypes = [P]
+    L.scone_check.restype = I
+    L.scone_table_destroy.argtypes = [P]
+    L.scone_table_destroy.restype = None
+    L.scone_table_info.argtypes = [P, ctypes.POINTER(I64), ctypes.POINTER(I64),
+                                   ctypes.POINTER(I32), ctypes.POINTER(I32)]
+    L.scone_table_info.restype = I
+    L.scone_strerror.argtypes = [I]
+    L.scone_strerror.restype = ctypes.c_char_p
+    return L
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise ImportError(
+                    f"{LIB_PATH} is missing: build it with paper_2502_01637_amd._build.build()")
+            _lib = _declare(ctypes.CDLL(LIB_PATH))
+        return _lib
+
+
+def _check(rc: int, what: str):
+    if rc != OK:
+        raise SconeError(rc, what)
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dev_i32(t: torch.Tensor, name: str, ndim: Optional[int] = None) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if t.dtype != torch.int32:
+        raise TypeError(f"{name} must be int32, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions")
+    return t
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None or t.numel() == 0 else t.data_ptr()
+
+
+class Table:
+    """A built f-gram dictionary (owns the library's table handle)."""
+
+    def __init__(self, handle: ctypes.c_void_p, device: torch.device):
+        self._h = handle
+        self.device = device
+        n, cap = ctypes.c_int64(), ctypes.c_int64()
+        ml, sb = ctypes.c_int32(), ctypes.c_int32()
+        _check(lib().scone_table_info(handle, ctypes.byref(n), ctypes.byref(cap),
+                                      ctypes.byref(ml), ctypes.byref(sb)), "scone_table_info")
+        self.n, self.capacity = n.value, cap.value
+        self.max_len, self.slot_bytes = ml.value, sb.value
+
+    @property
+    def handle(self) -> ctypes.c_void_p:
+        if self._h is None:
+            raise ValueError("table already destroyed")
+        return self._h
+
+    @property
+    def nbytes(self) -> int:
+        return self.capacity * self.slot_bytes
+
+    def close(self):
+        if self._h is not None:
+            lib().scone_table_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def build_fgram_table(fgrams: torch.Tensor, lengths: torch.Tensor, ids: torch.Tensor,
+                      max_load: float = 0.5, stream=None) -> Table:
+    """scone_build_fgram_table: fgrams [n, K] int32, lengths [n], ids [n] (device)."""
+    _dev_i32(fgrams, "fgrams", 2)
+    _dev_i32(lengths, "lengths", 1)
+    _dev_i32(ids, "ids", 1)
+    n, K = fgrams.shape
+    if lengths.numel() != n or ids.numel() != n:
+        raise ValueError("fgrams, lengths and ids disagree on n")
+    h = ctypes.c_void_p()
+    with torch.cuda.device(fgrams.device):
+        rc = lib().scone_build_fgram_table(_ptr(fgrams), _ptr(lengths), _ptr(ids), n, K,
+                                           float(max_load), _stream(stream), ctypes.byref(h))
+    _check(rc, "scone_build_fgram_table")
+    return Table(h, fgrams.device)
+
+
+def lookup(table: Table, token_ids: torch.Tensor, max_n: int,
+           fgram_ids: Optional[torch.Tensor] = None, match_len: Optional[torch.Tensor] = None,
+           want_len: bool = False, stream=None) -> Tuple[torch.Tensor, Optional[torch.Tensor]]:
+    """scone_lookup on token_ids [B, T]; returns (fgram_ids [B, T], match_len or None)."""
+    _dev_i32(token_ids, "token_ids", 2)
+    B, T = token_ids.shape
+    if fgram_ids is None:
+        fgram_ids = torch.empty((B, T), dtype=torch.int32, device=token_ids.device)
+    _dev_i32(fgram_ids, "fgram_ids")
+    if fgram_ids.numel() != B * T:
+        raise ValueError("fgram_ids has the wrong size")
+    if match_len is None and want_len:
+        match_len = torch.empty((B, T), dtype=torch.int8, device=token_ids.device)
+    if match_len is not None and (match_len.dtype != torch.int8 or match_len.numel() != B * T
+                                  or not match_len.is_contiguous()):
+        raise ValueError("match_len must be a contiguous int8 tensor of B*T elements")
+    with torch.cuda.device(token_ids.device):
+        rc = lib().scone_lookup(table.handle, _ptr(token_ids), B, T, int(max_n),
+                                _ptr(fgram_ids), _ptr(match_len), _stream(stream))
+    _check(rc, "scone_lookup")
+    return fgram_ids, match_len
+
+
+class HostRows:
+    """A row table in pinned host memory that kernels read over PCIe."""
+
+    def __init__(self, n_rows: int, row_shape, dtype: torch.dtype):
+        self.n_rows = int(n_rows)
+        self.row_shape = tuple(row_shape)
+        self.dtype = dtype
+        elem = torch.empty((), dtype=dtype).element_size()
+        per_row = elem
+        for s in self.row_shape:
+            per_row *= s
+        self.row_bytes = per_row
+        self.nbytes = self.n_rows * per_row
+        hp, dp = ctypes.c_void_p(), ctypes.c_void_p()
+        _check(lib().scone_host_alloc(max(self.nbytes, 1), ctypes.byref(hp), ctypes.byref(dp)),
+               "scone_host_alloc")
+        self.host_ptr, self.device_ptr = hp.value, dp.value
+        self._closed = False
+
+    def tensor(self) -> torch.Tensor:
+        """A CPU tensor view of the pinned memory (for filling and checking)."""
+        buf = (ctypes.c_uint8 * self.nbytes).from_address(self.host_ptr)
+        t = torch.frombuffer(buf, dtype=torch.uint8)
+        return t.view(self.dtype).view((self.n_rows,) + self.row_shape)
+
+    def close(self):
+        if not self._closed:
+            lib().scone_host_free(self.host_ptr)
+            self._closed = True
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def gather(fgram_ids: torch.Tensor, rows, out: Optional[torch.Tensor] = None,
+           stream=None) -> torch.Tensor:
+    """scone_gather: out[k] = rows[fgram_ids[k]]; rows is a CUDA tensor or HostRows."""
+    _dev_i32(fgram_ids, "fgram_ids")
+    n_tok = fgram_ids.numel()
+    if isinstance(rows, HostRows):
+        placement, base = PLACE_HOST, rows.device_ptr
+        n_rows, row_bytes, row_shape, dtype = rows.n_rows, rows.row_bytes, rows.row_shape, rows.dtype
+    else:
+        if not isinstance(rows, torch.Tensor) or rows.device.type != "cuda":
+            raise TypeError("rows must be a CUDA tensor or HostRows")
+        if not rows.is_contiguous() or rows.dim() < 1:
+            raise ValueError("rows must be a contiguous [n_rows, ...] tensor")
+        placement, base = PLACE_HBM, _ptr(rows)
+        n_rows, row_shape, dtype = rows.shape[0], tuple(rows.shape[1:]), rows.dtype
+        row_bytes = rows[0].numel() * rows.element_size() if n_rows else \
+            int(torch.Size(row_shape).numel()) * rows.element_size()
+    if out is None:
+        out = torch.empty(tuple(fgram_ids.shape) + row_shape, dtype=dtype,
+                          device=fgram_ids.device)
+    if not out.is_contiguous() or out.numel() * out.element_size() != n_tok * row_bytes:
+        raise ValueError("out must be contiguous with n_tok * row_bytes bytes")
+    with torch.cuda.device(fgram_ids.device):
+        rc = lib().scone_gather(_ptr(fgram_ids), n_tok, base, n_rows, row_bytes, _ptr(out),
+                                placement, _stream(stream))
+    _check(rc, "scone_gather")
+    return out
+
+
+def check(stream=None, device=None) -> int:
+    """scone_check: wait for the stream and return (and clear) the device's error status."""
+    dev = device if device is not None else torch.cuda.current_device()
+    with torch.cuda.device(dev):
+        return lib().scone_check(_stream(stream))
+
+
+def check_ok(stream=None):
+    _check(check(stream), "asynchronous call")

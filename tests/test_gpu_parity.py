@@ -1,0 +1,232 @@
+"""GPU path (through the C ABI) against the CPU oracle, bit for bit.
+
+Ids and match lengths are compared element by element with the oracle on the
+same seeded inputs; gathered rows are compared as raw bytes with the
+oracle's memcpy gather.  Sizes span several workgroup tiles with ragged
+tails; the edge cases cover empty inputs, window 1, windows wider than the
+table's K, 7-token f-grams (32-byte slots), extreme token values, unaligned
+row widths and every error the library reports.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2502_01637_amd as S
+from gpu_util import as_bytes, build_gpu, dev, device_rows
+from workloads import CONFIGS, make_workload, scaled, table_rows
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "alg1_worked_example.json")
+
+
+@pytest.fixture(autouse=True)
+def _clean_error_word():
+    if torch.cuda.is_available():
+        S.check()
+    yield
+    if torch.cuda.is_available():
+        assert S.check() == S.scone.OK, "a test left a device error behind"
+
+
+def pad(rows, width, fill=-1):
+    out = np.full((len(rows), width), fill, dtype=np.int32)
+    for k, r in enumerate(rows):
+        out[k, :len(r)] = r
+    return out
+
+
+def compare_lookup(w_fgrams, w_lengths, w_ids, X, max_n, max_load=0.5):
+    o = oracle.OracleTable(w_fgrams, w_lengths, w_ids)
+    exp_ids, exp_len = o.lookup(X, max_n)
+    tb = build_gpu(w_fgrams, w_lengths, w_ids, max_load)
+    ids, ml = S.lookup(tb, dev(X), max_n, want_len=True)
+    S.check_ok()
+    np.testing.assert_array_equal(ids.cpu().numpy(), exp_ids)
+    np.testing.assert_array_equal(ml.cpu().numpy(), exp_len)
+    return tb, exp_ids
+
+
+def test_worked_example_through_gpu():
+    g = json.load(open(GOLDEN))
+    fg = pad(g["fgrams"], 4)
+    ln = [len(r) for r in g["fgrams"]]
+    tb = build_gpu(fg, ln, g["ids"])
+    X = dev(np.array(g["tokens"], dtype=np.int32))
+    for max_n, exp in g["expected"].items():
+        ids, ml = S.lookup(tb, X, int(max_n), want_len=True)
+        assert ids.cpu().tolist() == exp["ids"], max_n
+        assert ml.cpu().tolist() == exp["len"], max_n
+
+
+def test_tiny_full_parity():
+    cfg = CONFIGS["tiny"]
+    w = make_workload(cfg)
+    tb, exp_ids = compare_lookup(w.fgrams, w.lengths, w.ids, w.tokens, cfg.max_n)
+    E = device_rows(cfg)
+    ids, _ = S.lookup(tb, dev(w.tokens), cfg.max_n)
+    out = S.gather(ids, E)
+    S.check_ok()
+    exp = oracle.gather(exp_ids, E.cpu().numpy())
+    assert as_bytes(out).tobytes() == exp.tobytes()
+
+
+@pytest.mark.parametrize("max_len", [2, 3, 5, 6, 7])
+@pytest.mark.parametrize("shape", [(1, 1), (3, 7), (2, 257), (5, 1000), (1, 4099)])
+def test_lookup_shapes_and_windows(max_len, shape):
+    V = 6  # tiny vocabulary: dense overlaps, every length matches somewhere
+    possible = sum(V ** n for n in range(2, max_len + 1))
+    cfg = scaled(CONFIGS["tiny"], V=V, n_fgrams=min(400, possible // 2), max_len=max_len,
+                 B=shape[0], T=shape[1], coverage=0.5)
+    w = make_workload(cfg, seed=11 * max_len + shape[1])
+    for max_n in sorted({1, 2, max_len - 1, max_len, max_len + 3}):
+        if max_n >= 1:
+            compare_lookup(w.fgrams, w.lengths, w.ids, w.tokens, max_n)
+
+
+def test_extreme_tokens_and_long_fgrams():
+    hi = 65535
+    rows = [[hi, 0], [0, hi, hi], [hi] * 7, [1, 2, 3, 4, 5, 6, 7], [7, 6, 5, 4, 3, 2],
+            [hi, hi, hi, hi, hi, hi], [0, 0]]
+    fg = pad(rows, 7)
+    ln = [len(r) for r in rows]
+    ids = [70000 + k for k in range(len(rows))]
+    X = np.array([[hi] * 9 + [0, hi, hi] + [1, 2, 3, 4, 5, 6, 7, 6, 5, 4, 3, 2] + [0] * 4],
+                 dtype=np.int32)
+    X = np.concatenate([X, X[:, ::-1]])
+    for max_n in range(1, 10):
+        compare_lookup(fg, ln, ids, X, max_n)
+
+
+def test_build_order_invariance():
+    cfg = scaled(CONFIGS["c3_10m_k5"], n_fgrams=50_000, B=4, T=3000)
+    w = make_workload(cfg)
+    perm = np.random.default_rng(3).permutation(len(w.lengths))
+    a = build_gpu(w.fgrams, w.lengths, w.ids)
+    b = build_gpu(w.fgrams[perm], w.lengths[perm], w.ids[perm])
+    X = dev(w.tokens)
+    ia, la = S.lookup(a, X, 5, want_len=True)
+    ib, lb = S.lookup(b, X, 5, want_len=True)
+    assert torch.equal(ia, ib) and torch.equal(la, lb)
+
+
+@pytest.mark.parametrize("max_load", [0.05, 0.5, 0.9])
+def test_load_factors(max_load):
+    cfg = scaled(CONFIGS["c2_1m"], n_fgrams=30_000, B=3, T=777)
+    w = make_workload(cfg)
+    tb, _ = compare_lookup(w.fgrams, w.lengths, w.ids, w.tokens, 3, max_load=max_load)
+    assert tb.n == 30_000 and tb.capacity >= 30_000 / max_load
+    assert tb.capacity & (tb.capacity - 1) == 0
+
+
+def test_empty_inputs():
+    tb = build_gpu(np.zeros((0, 3), np.int32), [], [])
+    assert tb.n == 0
+    X = dev(np.array([[5, 6, 7]], dtype=np.int32))
+    ids, ml = S.lookup(tb, X, 3, want_len=True)
+    assert ids.cpu().tolist() == [[5, 6, 7]] and ml.cpu().tolist() == [[1, 1, 1]]
+    for B, T in [(0, 5), (4, 0), (0, 0)]:
+        ids, _ = S.lookup(tb, torch.zeros((B, T), dtype=torch.int32, device="cuda"), 3)
+        assert ids.shape == (B, T)
+    E = torch.zeros((10, 8), dtype=torch.float32, device="cuda")
+    out = S.gather(torch.zeros(0, dtype=torch.int32, device="cuda"), E)
+    assert out.shape == (0, 8)
+
+
+@pytest.mark.parametrize("row_bytes", [1, 2, 3, 6, 12, 16, 48, 256, 2048, 4096, 4100])
+@pytest.mark.parametrize("offset", [0, 1, 4])
+def test_gather_row_widths_and_alignment(row_bytes, offset):
+    rng = np.random.default_rng(row_bytes + offset)
+    n_rows, n_tok = 300, 1537
+    table = rng.integers(0, 256, size=(n_rows, row_bytes), dtype=np.uint8)
+    ids = rng.integers(0, n_rows, size=n_tok).astype(np.int32)
+    exp = oracle.gather(ids, table)
+    E = dev(table)
+    buf = torch.empty(n_tok * row_bytes + offset, dtype=torch.uint8, device="cuda")
+    out = buf[offset:].view(n_tok, row_bytes)
+    S.gather(dev(ids), E, out=out)
+    S.check_ok()
+    assert out.cpu().numpy().tobytes() == exp.tobytes()
+
+
+def test_gather_keeps_special_bit_patterns():
+    E = torch.randn(64, 32, dtype=torch.float32)
+    E.view(torch.int32)[5, :5] = torch.tensor([0x80000000 - 2**32, 0x7F800000, 0x7FC01234,
+                                               0xFFC00001 - 2**32, 1], dtype=torch.int32)
+    Eb = torch.randn(64, 48).to(torch.bfloat16)
+    Eb.view(torch.int16)[7, :3] = torch.tensor([-32768, 0x7FC1, 0x7F81], dtype=torch.int16)
+    ids = np.array([5, 7, 5, 0, 63], dtype=np.int32)
+    for T in (E, Eb):
+        out = S.gather(dev(ids), T.cuda())
+        S.check_ok()
+        exp = oracle.gather(ids, T.view(torch.uint8).numpy())
+        assert as_bytes(out).tobytes() == exp.tobytes()
+
+
+def test_host_rows_gather():
+    cfg = scaled(CONFIGS["tiny"], d=96)
+    w = make_workload(cfg)
+    tb = build_gpu(w.fgrams, w.lengths, w.ids)
+    host = S.HostRows(cfg.n_rows, (cfg.d,), torch.float32)
+    try:
+        host.tensor().copy_(table_rows(cfg, range(cfg.n_rows)))
+        ids, _ = S.lookup(tb, dev(w.tokens), cfg.max_n)
+        out = S.gather(ids, host)
+        S.check_ok()
+        o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+        exp_ids, _ = o.lookup(w.tokens, cfg.max_n)
+        exp = oracle.gather(exp_ids, host.tensor().numpy())
+        assert as_bytes(out).tobytes() == exp.tobytes()
+    finally:
+        host.close()
+
+
+# ------------------------------------------------------------- errors ------
+
+def raises_code(code, fn, *a, **kw):
+    with pytest.raises(S.SconeError) as e:
+        fn(*a, **kw)
+    assert e.value.code == code, (e.value.code, code)
+
+
+def test_build_errors():
+    fg = pad([[1, 2], [2, 3], [3, 4, 5]], 3)
+    raises_code(S.scone.EDUP, build_gpu, pad([[1, 2], [9, 9], [1, 2]], 3), [2, 2, 2], [10, 11, 12])
+    raises_code(S.scone.ELEN, build_gpu, fg, [2, 1, 3], [10, 11, 12])
+    raises_code(S.scone.ELEN, build_gpu, fg, [2, 2, 4], [10, 11, 12])
+    raises_code(S.scone.EID, build_gpu, fg, [2, 2, 3], [10, -11, 12])
+    raises_code(S.scone.ETOKEN, build_gpu, pad([[1, 70000]], 3), [2], [10])
+    raises_code(S.scone.ETOKEN, build_gpu, pad([[-1, 2]], 3), [2], [10])
+    raises_code(S.scone.EINVAL, build_gpu, fg, [2, 2, 3], [10, 11, 12], max_load=0.95)
+    raises_code(S.scone.EINVAL, build_gpu, pad([[1, 2]], 8), [2], [10])
+    # many duplicates among many keys, one key repeated once
+    rng = np.random.default_rng(0)
+    base = rng.integers(0, 60000, size=(20000, 3)).astype(np.int32)
+    base = np.unique(base, axis=0)
+    dup = np.concatenate([base, base[1234:1235]])
+    raises_code(S.scone.EDUP, build_gpu, dup, np.full(len(dup), 3), np.arange(len(dup)) + 5)
+
+
+def test_lookup_and_gather_errors_raise_through_check():
+    tb = build_gpu(pad([[1, 2]], 3), [2], [10])
+    X = dev(np.array([[1, 2, 65536, 3]], dtype=np.int32))
+    ids, _ = S.lookup(tb, X, 3)
+    assert S.check() == S.scone.ETOKEN
+    assert S.check() == S.scone.OK  # cleared
+    X = dev(np.array([[1, 2, -5]], dtype=np.int32))
+    S.lookup(tb, X, 3)
+    assert S.check() == S.scone.ETOKEN
+    E = torch.arange(40, dtype=torch.float32, device="cuda").view(10, 4) + 1
+    out = S.gather(dev(np.array([1, 10, 3, -1], dtype=np.int32)), E)
+    assert S.check() == S.scone.EROW
+    got = out.cpu()
+    assert torch.equal(got[0], E[1].cpu()) and torch.equal(got[2], E[3].cpu())
+    assert (got[1] == 0).all() and (got[3] == 0).all()
+    empty_rows = torch.zeros((0, 4), dtype=torch.float32, device="cuda")
+    S.gather(dev(np.array([0], dtype=np.int32)), empty_rows)
+    assert S.check() == S.scone.EROW
+    raises_code(S.scone.EINVAL, S.lookup, tb, X, 0)

@@ -109,53 +109,87 @@ def zipf_cdf(V: int, s: float = ZIPF_S) -> np.ndarray:
     return c
 
 
+_GUIDE_BITS = 21
+_guides: dict = {}
+
+
+def _guide(cdf: np.ndarray) -> np.ndarray:
+    """guide[b] = smallest rank k with cdf[k] > b / 2^21 (an index for the search)."""
+    key = (len(cdf), float(cdf[0]))
+    g = _guides.get(key)
+    if g is None:
+        M = 1 << _GUIDE_BITS
+        g = np.searchsorted(cdf, np.arange(M, dtype=np.float64) / M, side="right")
+        _guides[key] = g
+    return g
+
+
 def zipf_tokens(rng: np.random.Generator, cdf: np.ndarray, size) -> np.ndarray:
-    """Inverse-CDF draw of bounded Zipf ranks, returned as token ids (rank-1)."""
-    u = rng.random(size)
-    k = np.searchsorted(cdf, u, side="right")
-    return np.minimum(k, len(cdf) - 1).astype(np.int32)
+    """Inverse-CDF draw of bounded Zipf ranks, returned as token ids (rank-1).
+
+    The result is the smallest k with cdf[k] > u, found from a guide table
+    and a short forward scan (the same value as a binary search).
+    """
+    u = rng.random(size).reshape(-1)
+    k = _guide(cdf)[(u * (1 << _GUIDE_BITS)).astype(np.int64)]
+    last = len(cdf) - 1
+    todo = np.nonzero(cdf[np.minimum(k, last)] <= u)[0]
+    while todo.size:
+        k[todo] += 1
+        todo = todo[(k[todo] < last) & (cdf[np.minimum(k[todo], last)] <= u[todo])]
+    return np.minimum(k, last).astype(np.int32).reshape(size)
 
 
 # --------------------------------------------------------------- f-grams ----
 
-def _first_occurrence(rows: np.ndarray, lens: np.ndarray) -> np.ndarray:
-    """Indices (ascending) of the first occurrence of each distinct f-gram.
+def _fingerprint(rows: np.ndarray, lens: np.ndarray) -> np.ndarray:
+    """64-bit fingerprint of (length, tokens) for duplicate rejection.
 
-    Rows are padded with -1 past their length, so (lens, rows) identifies the
-    f-gram exactly.  A stable lexicographic sort keeps the earliest draw of
-    each group first.
+    Equal f-grams always share a fingerprint; two different f-grams share one
+    with negligible probability, and then one of them is merely dropped, so
+    the kept set is always a set of distinct f-grams.
     """
-    keys = [rows[:, j] for j in range(rows.shape[1] - 1, -1, -1)] + [lens]
-    order = np.lexsort(keys)
-    srt = np.column_stack([lens[order], rows[order]])
-    new = np.ones(len(order), dtype=bool)
-    if len(order) > 1:
-        new[1:] = np.any(srt[1:] != srt[:-1], axis=1)
-    return np.sort(order[new])
+    with np.errstate(over="ignore"):
+        h = lens.astype(np.uint64) * np.uint64(0x9E3779B97F4A7C15)
+        for j in range(rows.shape[1]):
+            h ^= (rows[:, j].astype(np.int64) + 1).astype(np.uint64)
+            h *= np.uint64(0xFF51AFD7ED558CCD)
+            h ^= h >> np.uint64(29)
+        h *= np.uint64(0xC4CEB9FE1A85EC53)
+        h ^= h >> np.uint64(32)
+    return h
 
 
 def make_fgrams(rng: np.random.Generator, cdf: np.ndarray, n: int,
                 min_len: int, max_len: int):
-    """Draw ``n`` distinct f-grams.
+    """Draw ``n`` distinct f-grams (first occurrence kept, draw order preserved).
 
     Returns (fgrams [n, max_len] int32 padded with -1, lengths [n] int32).
     """
     rows = np.empty((0, max_len), dtype=np.int32)
     lens = np.empty(0, dtype=np.int32)
-    batch = max(1024, int(n * 1.2))
+    fps = np.empty(0, dtype=np.uint64)
+    batch = max(1024, int(n * 1.1))
+    rounds = 0
     while len(lens) < n:
+        rounds += 1
+        if rounds > 200:
+            raise ValueError(f"cannot draw {n} distinct f-grams of length "
+                             f"{min_len}..{max_len} from this vocabulary")
         bl = rng.integers(min_len, max_len + 1, size=batch).astype(np.int32)
         bt = zipf_tokens(rng, cdf, (batch, max_len))
         bt[np.arange(max_len)[None, :] >= bl[:, None]] = -1
         have = len(lens)
-        rows = np.concatenate([rows, bt])
-        lens = np.concatenate([lens, bl])
-        keep = _first_occurrence(rows, lens)
-        rows, lens = rows[keep], lens[keep]
-        gained = len(lens) - have
+        allfp = np.concatenate([fps, _fingerprint(bt, bl)])
+        _, first = np.unique(allfp, return_index=True)  # stable: earliest draw wins
+        first.sort()
+        new = first[first >= have] - have
+        rows = np.concatenate([rows, bt[new]])
+        lens = np.concatenate([lens, bl[new]])
+        fps = np.concatenate([fps, allfp[have:][new]])
         deficit = n - len(lens)
         if deficit > 0:
-            rate = max(gained / batch, 0.01)
+            rate = max(len(new) / batch, 0.01)
             batch = max(1024, int(deficit / rate * 1.1))
     return np.ascontiguousarray(rows[:n]), np.ascontiguousarray(lens[:n])
 
