@@ -1,0 +1,277 @@
+#!/usr/bin/env python3
+"""Benchmark of the f-gram embedding hot path on one MI355X.
+
+One step is one pass of the whole path over one [B, T] batch already resident
+in HBM: the longest-suffix lookup (scone_lookup) followed by the row gather
+(scone_gather).  The table build is offline and not timed.  Prints one JSON
+line with tokens/s, the gather's achieved bandwidth against the HBM peak, and
+the CPU oracle timed on a bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "tokens/sec and gather GB/s (% of HBM peak) for f-gram lookup+gather, 1 MI355X"
+HBM_PEAK_GBPS = 8000.0
+DEFAULT_CONFIG = "c2_1m"
+N_BATCHES = 4
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def describe(cfg) -> str:
+    return (f"{cfg.name}: vocab {cfg.V} Zipf(1.1), {cfg.n_fgrams} f-grams of length "
+            f"{cfg.min_len}..{cfg.max_len}, table {cfg.n_rows}x{cfg.d} {cfg.dtype} in "
+            f"{cfg.placement}, queries {cfg.B}x{cfg.T}, {int(cfg.coverage * 100)}% planted "
+            f"coverage, max_n={cfg.max_n}")
+
+
+def source_sha(name: str) -> str:
+    p = os.path.join(ROOT, "paper_2502_01637_amd", "csrc", name)
+    return hashlib.sha1(open(p, "rb").read()).hexdigest()[:12]
+
+
+def measured_traffic(config: str, kernel_src: str):
+    """HBM bytes per gather launch from the committed rocprofv3 counter summary,
+    or None when there is none for this kernel source."""
+    path = os.path.join(ROOT, "profiles", f"gather_{config}_traffic.md")
+    if not os.path.exists(path):
+        return None
+    m = re.search(r"^TRAFFIC (\{.*\})\s*$", open(path).read(), re.M)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("source_sha1") != source_sha(kernel_src):
+        return None
+    return rec
+
+
+def cpu_baseline(cfg, w, X0, E, gpu_ids, gpu_out, min_seconds: float):
+    """Time the oracle (single-threaded) on batch 0, repeated until min_seconds."""
+    import torch
+    import oracle
+    from workloads import table_rows
+    t0 = time.perf_counter()
+    o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+    build_s = time.perf_counter() - t0
+    exp_ids, exp_len = o.lookup(X0, cfg.max_n)
+    full = cfg.n_rows * cfg.row_bytes <= (4 << 30)
+    if full:
+        # the whole row table in host memory, as the paper's in-memory store
+        host = E.cpu()
+        uniq = None
+    else:
+        # only the rows this batch references (the full table is not copied to
+        # the host); the id remap to that compact table is timed with the gather
+        uniq = np.unique(exp_ids)
+        host = table_rows(cfg, torch.from_numpy(uniq.astype(np.int64)), device="cuda").cpu()
+    host_np = host.view(torch.uint8).numpy()
+    passes, elapsed = 0, 0.0
+    while elapsed < min_seconds or passes == 0:
+        t = time.perf_counter()
+        ids_p, _ = o.lookup(X0, cfg.max_n)
+        if uniq is not None:
+            ids_p = np.searchsorted(uniq, ids_p).astype(np.int32)
+        out = oracle.gather(ids_p, host_np)
+        elapsed += time.perf_counter() - t
+        passes += 1
+    what = ("the full host table" if full else
+            f"a compact host table of the {len(uniq)} referenced rows (id remap timed)")
+    parity_ids = bool(np.array_equal(gpu_ids, exp_ids))
+    parity_rows = bool(gpu_out.view(torch.uint8).cpu().numpy().reshape(out.shape).tobytes()
+                       == out.tobytes())
+    return ({"value": passes * cfg.n_tok / elapsed, "unit": "tokens/s", "cores": 1,
+             "kind": "oracle",
+             "sample": f"batch 0 ({cfg.n_tok} tokens) of {describe(cfg)}; {passes} full "
+                       f"passes of lookup + memcpy gather from {what}; dictionary build "
+                       f"({build_s:.1f} s) not timed",
+             "seconds": round(elapsed, 3), "build_seconds": round(build_s, 3)},
+            {"ids_bit_exact": parity_ids, "rows_bit_exact": parity_rows,
+             "positions": int(cfg.n_tok)}, exp_len)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default=DEFAULT_CONFIG)
+    ap.add_argument("--max-load", type=float, default=0.5)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="also run a plain device copy of MIB MiB (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              f"(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2502_01637_amd as S
+    from workloads import CONFIGS, make_workload, query_batches, fill_table, torch_dtype, \
+        match_stats
+
+    cfg = CONFIGS[args.config]
+    if cfg.placement != "hbm" or cfg.decode:
+        print(f"config {cfg.name} is not an HBM prefill workload", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    log("workload:", describe(cfg))
+
+    t = time.perf_counter()
+    w = make_workload(cfg)
+    batches_np = query_batches(w, N_BATCHES)
+    log(f"generated in {time.perf_counter() - t:.1f} s")
+    fg = torch.from_numpy(w.fgrams).to(dev)
+    ln = torch.from_numpy(w.lengths).to(dev)
+    idv = torch.from_numpy(w.ids).to(dev)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    table = S.build_fgram_table(fg, ln, idv, max_load=args.max_load)
+    build_s = time.perf_counter() - t
+    del fg, ln, idv
+    E = torch.empty((cfg.n_rows, cfg.d), dtype=torch_dtype(cfg), device=dev)
+    fill_table(cfg, E)
+    X = [torch.from_numpy(b).to(dev) for b in batches_np]
+    fid = torch.empty((cfg.B, cfg.T), dtype=torch.int32, device=dev)
+    out = torch.empty((cfg.B, cfg.T, cfg.d), dtype=E.dtype, device=dev)
+    torch.cuda.synchronize()
+    log(f"table: {table.n} f-grams, {table.capacity} slots x {table.slot_bytes} B, "
+        f"build {build_s * 1e3:.1f} ms; rows {E.numel() * E.element_size() / 1e9:.2f} GB")
+
+    def step(k):
+        S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
+        S.gather(fid, E, out=out)
+
+    for k in range(args.warmup):
+        step(k)
+    rc = S.check()
+    if rc != 0:
+        raise SystemExit(f"device error after warmup: status {rc}")
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(K):
+        e = ev[k]
+        e[0].record()
+        S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
+        e[1].record()
+        S.gather(fid, E, out=out)
+        e[2].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    rc = S.check()
+    if rc != 0:
+        raise SystemExit(f"device error in timed region: status {rc}")
+    lookup_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    gather_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    gpu_span_ms = ev[0][0].elapsed_time(ev[-1][2])
+
+    gather_bytes = cfg.gather_bytes()
+    achieved = gather_bytes / (gather_ms * 1e-3) / 1e9
+    value = cfg.n_tok * K / wall
+
+    # Uniform-random-id control at the same shape: no Zipf reuse to help the caches.
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(cfg.seed)
+    uid = torch.randint(0, cfg.n_rows, (cfg.B, cfg.T), dtype=torch.int32, device=dev,
+                        generator=gen)
+    for _ in range(3):
+        S.gather(uid, E, out=out)
+    ue = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ue[0].record()
+    for _ in range(K):
+        S.gather(uid, E, out=out)
+    ue[1].record()
+    torch.cuda.synchronize()
+    uniform_ms = ue[0].elapsed_time(ue[1]) / K
+
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    # Batch 0 once more for the parity check and the match statistics.
+    fid0, ml0 = S.lookup(table, X[0], cfg.max_n, want_len=True)
+    out0 = S.gather(fid0, E)
+    if S.check() != 0:
+        raise SystemExit("device error in parity pass")
+    torch.cuda.synchronize()
+
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": wall * 1e3 / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded Zipf(1.1) tokens, planted f-grams, counter-based rows)",
+        "config": {"workload": describe(cfg), "B": cfg.B, "T": cfg.T, "tokens": cfg.n_tok,
+                   "n_fgrams": cfg.n_fgrams, "max_n": cfg.max_n, "d": cfg.d,
+                   "row_bytes": cfg.row_bytes, "placement": "hbm",
+                   "hash_slots": table.capacity, "slot_bytes": table.slot_bytes,
+                   "rotating_batches": N_BATCHES},
+        "gather_GBps": achieved,
+        "gather_pct_hbm_peak": 100.0 * achieved / HBM_PEAK_GBPS,
+        "lookup_us": lookup_ms * 1e3,
+        "gather_us": gather_ms * 1e3,
+        "gpu_span_ms_per_step": gpu_span_ms / K,
+        "uniform_id_gather": {"us": uniform_ms * 1e3,
+                              "GBps": gather_bytes / (uniform_ms * 1e-3) / 1e9,
+                              "pct_hbm_peak": 100.0 * gather_bytes / (uniform_ms * 1e-3) / 1e9
+                              / HBM_PEAK_GBPS},
+    }
+    traffic = measured_traffic(cfg.name, "gather.hip")
+    result["roofline"] = {
+        "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+        "frac": achieved / HBM_PEAK_GBPS,
+        "traffic": None if traffic is None else traffic["traffic_bytes_per_launch"],
+        "kernel": "k_gather (scone_gather)",
+        "algorithmic_bytes_per_launch": gather_bytes,
+    }
+    ml = ml0.cpu().numpy()
+    result["match"] = match_stats(ml, cfg.max_n)
+    result["build_ms"] = build_s * 1e3
+
+    if not args.no_cpu_baseline:
+        cb, parity, exp_len = cpu_baseline(cfg, w, batches_np[0], E, fid0.cpu().numpy(), out0,
+                                           args.cpu_seconds)
+        parity["match_len_bit_exact"] = bool(np.array_equal(ml, exp_len))
+        result["cpu_baseline"] = cb
+        result["parity"] = parity
+    else:
+        result["cpu_baseline"] = None
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -345,3 +345,16 @@ def match_stats(lens: np.ndarray, max_n: int) -> dict:
     return {"hist": {int(k): int(v) for k, v in enumerate(h) if k >= 1 and v},
             "matched_frac": float((lens >= 2).sum()) / tot,
             "mean_len": float(lens.astype(np.float64).mean()) if lens.size else 0.0}
+
+
+def query_batches(w: Workload, n: int):
+    """``n`` query matrices of the workload's shape: the workload's own first,
+    then fresh draws from the same f-gram set (rotating batches keep one
+    step's rows from being served out of the caches filled by the last)."""
+    out = [w.tokens]
+    cdf = zipf_cdf(w.cfg.V)
+    for k in range(1, n):
+        rng = np.random.Generator(np.random.PCG64([w.cfg.seed, k]))
+        X, _, _ = make_queries(rng, cdf, w.fgrams, w.lengths, w.cfg.B, w.cfg.T, w.cfg.coverage)
+        out.append(X)
+    return out
