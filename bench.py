@@ -46,10 +46,10 @@ def source_sha(name: str) -> str:
     return hashlib.sha1(open(p, "rb").read()).hexdigest()[:12]
 
 
-def measured_traffic(config: str, kernel_src: str):
-    """HBM bytes per gather launch from the committed rocprofv3 counter summary,
-    or None when there is none for this kernel source."""
-    path = os.path.join(ROOT, "profiles", f"gather_{config}_traffic.md")
+def measured_traffic(config: str, kernel: str, kernel_src: str):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary, or None when there is none for this kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{config}_traffic.md")
     if not os.path.exists(path):
         return None
     m = re.search(r"^TRAFFIC (\{.*\})\s*$", open(path).read(), re.M)
@@ -61,7 +61,7 @@ def measured_traffic(config: str, kernel_src: str):
     return rec
 
 
-def cpu_baseline(cfg, w, X0, E, gpu_ids, gpu_out, min_seconds: float):
+def cpu_baseline(cfg, w, X0, E, gpu_ids, gpu_outs, min_seconds: float):
     """Time the oracle (single-threaded) on batch 0, repeated until min_seconds."""
     import torch
     import oracle
@@ -93,16 +93,16 @@ def cpu_baseline(cfg, w, X0, E, gpu_ids, gpu_out, min_seconds: float):
     what = ("the full host table" if full else
             f"a compact host table of the {len(uniq)} referenced rows (id remap timed)")
     parity_ids = bool(np.array_equal(gpu_ids, exp_ids))
-    parity_rows = bool(gpu_out.view(torch.uint8).cpu().numpy().reshape(out.shape).tobytes()
-                       == out.tobytes())
+    parity_rows = [bool(g.view(torch.uint8).cpu().numpy().reshape(out.shape).tobytes()
+                        == out.tobytes()) for g in gpu_outs]
     return ({"value": passes * cfg.n_tok / elapsed, "unit": "tokens/s", "cores": 1,
              "kind": "oracle",
              "sample": f"batch 0 ({cfg.n_tok} tokens) of {describe(cfg)}; {passes} full "
                        f"passes of lookup + memcpy gather from {what}; dictionary build "
                        f"({build_s:.1f} s) not timed",
              "seconds": round(elapsed, 3), "build_seconds": round(build_s, 3)},
-            {"ids_bit_exact": parity_ids, "rows_bit_exact": parity_rows,
-             "positions": int(cfg.n_tok)}, exp_len)
+            {"ids_bit_exact": parity_ids, "fused_rows_bit_exact": parity_rows[0],
+             "split_rows_bit_exact": parity_rows[1], "positions": int(cfg.n_tok)}, exp_len)
 
 
 def main():
@@ -157,38 +157,54 @@ def main():
     log(f"table: {table.n} f-grams, {table.capacity} slots x {table.slot_bytes} B, "
         f"build {build_s * 1e3:.1f} ms; rows {E.numel() * E.element_size() / 1e9:.2f} GB")
 
-    def step(k):
+    def split_step(k):
         S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
         S.gather(fid, E, out=out)
 
-    for k in range(args.warmup):
-        step(k)
-    rc = S.check()
-    if rc != 0:
-        raise SystemExit(f"device error after warmup: status {rc}")
+    def fused_step(k):
+        S.embed(table, X[k % N_BATCHES], cfg.max_n, E, out=out)
 
     K = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(K):
-        e = ev[k]
-        e[0].record()
-        S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
-        e[1].record()
-        S.gather(fid, E, out=out)
-        e[2].record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    rc = S.check()
-    if rc != 0:
-        raise SystemExit(f"device error in timed region: status {rc}")
-    lookup_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
-    gather_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
-    gpu_span_ms = ev[0][0].elapsed_time(ev[-1][2])
+
+    def timed(path):
+        """W warm-up steps, then K timed steps between two synchronisations.
+        Returns (wall seconds, per-kernel mean ms list)."""
+        for k in range(args.warmup):
+            (split_step if path == "split" else fused_step)(k)
+        rc = S.check()
+        if rc != 0:
+            raise SystemExit(f"device error after warmup ({path}): status {rc}")
+        nk = 2 if path == "split" else 1
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(nk + 1)] for _ in range(K)]
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(K):
+            e = ev[k]
+            e[0].record()
+            if path == "split":
+                S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
+                e[1].record()
+                S.gather(fid, E, out=out)
+            else:
+                S.embed(table, X[k % N_BATCHES], cfg.max_n, E, out=out)
+            e[nk].record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        rc = S.check()
+        if rc != 0:
+            raise SystemExit(f"device error in timed region ({path}): status {rc}")
+        per = [float(np.mean([e[i].elapsed_time(e[i + 1]) for e in ev])) for i in range(nk)]
+        return wall, per
+
+    # The split path first (lookup and gather kernels), then the headline
+    # fused path, each over the same K steps.
+    split_wall, (lookup_ms, gather_ms) = timed("split")
+    wall, (embed_ms,) = timed("fused")
 
     gather_bytes = cfg.gather_bytes()
     achieved = gather_bytes / (gather_ms * 1e-3) / 1e9
+    embed_bytes = cfg.n_tok * (4 + 2 * cfg.row_bytes)
+    embed_achieved = embed_bytes / (embed_ms * 1e-3) / 1e9
     value = cfg.n_tok * K / wall
 
     # Uniform-random-id control at the same shape: no Zipf reuse to help the caches.
@@ -198,6 +214,7 @@ def main():
                         generator=gen)
     for _ in range(3):
         S.gather(uid, E, out=out)
+    torch.cuda.synchronize()
     ue = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     ue[0].record()
     for _ in range(K):
@@ -218,6 +235,7 @@ def main():
     # Batch 0 once more for the parity check and the match statistics.
     fid0, ml0 = S.lookup(table, X[0], cfg.max_n, want_len=True)
     out0 = S.gather(fid0, E)
+    out0f = S.embed(table, X[0], cfg.max_n, E)
     if S.check() != 0:
         raise SystemExit("device error in parity pass")
     torch.cuda.synchronize()
@@ -240,31 +258,38 @@ def main():
                    "row_bytes": cfg.row_bytes, "placement": "hbm",
                    "hash_slots": table.capacity, "slot_bytes": table.slot_bytes,
                    "rotating_batches": N_BATCHES},
-        "gather_GBps": achieved,
-        "gather_pct_hbm_peak": 100.0 * achieved / HBM_PEAK_GBPS,
-        "lookup_us": lookup_ms * 1e3,
-        "gather_us": gather_ms * 1e3,
-        "gpu_span_ms_per_step": gpu_span_ms / K,
+        "path": "fused lookup+gather (scone_embed)",
+        "embed_us": embed_ms * 1e3,
+        "embed_GBps": embed_achieved,
+        "embed_pct_hbm_peak": 100.0 * embed_achieved / HBM_PEAK_GBPS,
+        "split_path": {"tokens_per_s": cfg.n_tok * K / split_wall,
+                       "ms_per_step": split_wall * 1e3 / K,
+                       "lookup_us": lookup_ms * 1e3, "gather_us": gather_ms * 1e3,
+                       "gather_GBps": achieved,
+                       "gather_pct_hbm_peak": 100.0 * achieved / HBM_PEAK_GBPS},
         "uniform_id_gather": {"us": uniform_ms * 1e3,
                               "GBps": gather_bytes / (uniform_ms * 1e-3) / 1e9,
                               "pct_hbm_peak": 100.0 * gather_bytes / (uniform_ms * 1e-3) / 1e9
                               / HBM_PEAK_GBPS},
     }
-    traffic = measured_traffic(cfg.name, "gather.hip")
+    traffic = measured_traffic(cfg.name, "embed", "embed.hip")
     result["roofline"] = {
-        "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-        "frac": achieved / HBM_PEAK_GBPS,
+        "bound": "hbm", "achieved": embed_achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+        "frac": embed_achieved / HBM_PEAK_GBPS,
         "traffic": None if traffic is None else traffic["traffic_bytes_per_launch"],
-        "kernel": "k_gather (scone_gather)",
-        "algorithmic_bytes_per_launch": gather_bytes,
+        "kernel": "k_embed (scone_embed)",
+        "algorithmic_bytes_per_launch": embed_bytes,
     }
+    gtraffic = measured_traffic(cfg.name, "gather", "gather.hip")
+    result["split_path"]["gather_traffic"] = (None if gtraffic is None
+                                              else gtraffic["traffic_bytes_per_launch"])
     ml = ml0.cpu().numpy()
     result["match"] = match_stats(ml, cfg.max_n)
     result["build_ms"] = build_s * 1e3
 
     if not args.no_cpu_baseline:
-        cb, parity, exp_len = cpu_baseline(cfg, w, batches_np[0], E, fid0.cpu().numpy(), out0,
-                                           args.cpu_seconds)
+        cb, parity, exp_len = cpu_baseline(cfg, w, batches_np[0], E, fid0.cpu().numpy(),
+                                           [out0f, out0], args.cpu_seconds)
         parity["match_len_bit_exact"] = bool(np.array_equal(ml, exp_len))
         result["cpu_baseline"] = cb
         result["parity"] = parity

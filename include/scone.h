@@ -134,6 +134,50 @@ int scone_gather(const int32_t* fgram_ids, int64_t n_tok, const void* rows,
                  void* stream);
 
 /*
+ * Fused lookup + gather (the whole inference branch of Algorithm 1 in one
+ * kernel): produces exactly what scone_lookup followed by scone_gather
+ * produces, without the ids passing through memory in between.
+ *
+ *  token_ids, B, T, max_n   as for scone_lookup.
+ *  rows, n_rows, row_bytes, placement   as for scone_gather.
+ *  out        [B, T, row_bytes] device output.
+ *  fgram_ids  [B, T] int32 output, or NULL when not wanted.
+ *  match_len  [B, T] int8 output, or NULL.
+ *
+ * Errors as for scone_lookup and scone_gather.  Asynchronous on `stream`.
+ */
+int scone_embed(const scone_table_t* table, const int32_t* token_ids, int64_t B, int64_t T,
+                int32_t max_n, const void* rows, int64_t n_rows, int64_t row_bytes,
+                int32_t placement, void* out, int32_t* fgram_ids, int8_t* match_len,
+                void* stream);
+
+/*
+ * One decoding step for S sequences (inference emits one token per step per
+ * sequence; Section 4.3 measures per-token latency this way).  Sequence s
+ * appends new_tok[s] to its rolling context and gets the embedding of the
+ * longest f-gram ending at that token (Algorithm 1 at the newest position).
+ *
+ *  ctx        [S, ctx_cap] int32, in/out: the last ctx_len[s] tokens of
+ *             sequence s, oldest first (the rest is ignored).  Rewritten
+ *             with the last min(ctx_cap, ctx_len[s] + 1) tokens.
+ *  ctx_len    [S] int32, in/out; 0 for a new sequence.  Values outside
+ *             [0, ctx_cap] are treated as the nearest bound.
+ *  ctx_cap    context capacity, in [min(max_n, K) - 1, 63]; with at least
+ *             max_n - 1 tokens kept, step s of a sequence gives the same id
+ *             and row as scone_lookup at position s of the whole sequence.
+ *  new_tok    [S] int32 tokens in [0, SCONE_TOKEN_LIMIT).
+ *  rows ...   as for scone_gather; out is [S, row_bytes].
+ *  fgram_ids  [S] int32 output, or NULL; match_len [S] int8 or NULL.
+ *
+ * Asynchronous on `stream`.  Calls for the same sequences must be ordered
+ * (the context is read and rewritten in place).
+ */
+int scone_decode_step(const scone_table_t* table, int32_t* ctx, int32_t* ctx_len,
+                      int32_t ctx_cap, const int32_t* new_tok, int64_t S, int32_t max_n,
+                      const void* rows, int64_t n_rows, int64_t row_bytes, int32_t placement,
+                      void* out, int32_t* fgram_ids, int8_t* match_len, void* stream);
+
+/*
  * Allocate `bytes` of pinned host memory that kernels can read over PCIe
  * (the off-accelerator row store of Section 4.3).  *host_ptr receives the
  * host address, *device_ptr the address to pass to scone_gather with

@@ -5,8 +5,8 @@ the longest-suffix lookup and the row gather as HIP kernels; ``scone`` is its
 Python binding.
 """
 from . import scone
-from .scone import (SconeError, Table, HostRows, build_fgram_table, lookup, gather, check,
-                    check_ok)
+from .scone import (SconeError, Table, HostRows, build_fgram_table, lookup, gather, embed,
+                    decode_step, check, check_ok)
 
 __all__ = ["scone", "SconeError", "Table", "HostRows", "build_fgram_table", "lookup", "gather",
-           "check", "check_ok"]
+           "embed", "decode_step", "check", "check_ok"]

@@ -109,6 +109,15 @@ hipError_t launch_gather(const int32_t* ids, int64_t n_tok, const void* rows, in
 }
 
 }  // namespace
+
+hipError_t launch_zero_rows(void* out, int64_t bytes, unsigned* err, hipStream_t st) {
+    const int64_t grid = (bytes + kGatherThreads - 1) / kGatherThreads;
+    if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(k_zero<uint8_t>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, bytes,
+                       static_cast<uint8_t*>(out), err);
+    return hipGetLastError();
+}
+
 }  // namespace scone
 
 extern "C" int scone_gather(const int32_t* fgram_ids, int64_t n_tok, const void* rows,

@@ -9,60 +9,31 @@
 // members).  A wave-wide ballot of the hit flags then gives, per group, the
 // lowest hitting lane, i.e. the longest matching f-gram, and a lane shuffle
 // moves its id to the group's first lane, which writes the result.
-#include "scone_internal.h"
+#include "tile_lookup.h"
 
 namespace scone {
 namespace {
 
-constexpr int kLookupThreads = 256;
-constexpr int kMaxHalo = SCONE_MAX_FGRAM_LEN - 1;
-
 template <int SB, int G>
-__global__ __launch_bounds__(kLookupThreads) void k_lookup(
+__global__ __launch_bounds__(kTileThreads) void k_lookup(
     const typename SlotOps<SB>::Slot* __restrict__ slots, uint64_t mask,
     const int32_t* __restrict__ X, int64_t T, int max_n, int64_t tiles_per_row,
     int32_t* __restrict__ ids_out, int8_t* __restrict__ len_out, unsigned* __restrict__ err) {
-    constexpr int kTile = kLookupThreads / G;  // positions per workgroup
-    __shared__ int32_t s_tok[kTile + kMaxHalo];
-
+    constexpr int P = TileShape<G>::kPositions;
+    __shared__ int32_t s_tok[P + kMaxHalo];
     const int64_t b = blockIdx.x / tiles_per_row;
-    const int64_t t0 = (blockIdx.x - b * tiles_per_row) * (int64_t)kTile;
-    const int32_t* row = X + b * T;
-    const int halo = max_n - 1;
-    for (int i = threadIdx.x; i < kTile + halo; i += kLookupThreads) {
-        const int64_t t = t0 - halo + i;
-        s_tok[i] = (t >= 0 && t < T) ? row[t] : 0;
-    }
+    const int64_t t0 = (blockIdx.x - b * tiles_per_row) * (int64_t)P;
+    stage_tokens<G>(s_tok, X + b * T, T, t0, max_n - 1);
     __syncthreads();
-
-    const int p = threadIdx.x / G;  // position within the tile
-    const int j = threadIdx.x % G;  // lane within the position's group
-    const int64_t t = t0 + p;
-    const int n = max_n - j;        // suffix length this lane tests
-    bool hit = false;
-    int32_t id = 0;
-    if (t < T && n >= 2 && (int64_t)n <= t + 1) {
-        const int32_t* win = s_tok + p + halo - n + 1;  // X[b, t-n+1 .. t]
-        bool ok = true;
-#pragma unroll
-        for (int i = 0; i < SCONE_MAX_FGRAM_LEN; ++i)
-            if (i < n) ok &= (win[i] >= 0) & (win[i] < SCONE_TOKEN_LIMIT);
-        if (ok) hit = probe<SB>(slots, mask, pack_key(win, n), id);
-    }
-
-    // Longest hit of each group: lowest set bit among the group's lanes.
-    const unsigned long long m = __ballot(hit);
-    const int lane = threadIdx.x & 63;
-    const int base = lane & ~(G - 1);
-    const unsigned gm = (unsigned)(m >> base) & ((1u << G) - 1u);
-    const int jb = gm ? __ffs(gm) - 1 : 0;
-    const int32_t best = __shfl(id, base + jb);
-
-    if (j == 0 && t < T) {
-        const int32_t tok = s_tok[p + halo];
-        if (tok < 0 || tok >= SCONE_TOKEN_LIMIT) atomicOr(err, err_bit(SCONE_ETOKEN));
-        ids_out[b * T + t] = gm ? best : tok;
-        if (len_out) len_out[b * T + t] = (int8_t)(gm ? max_n - jb : 1);
+    int32_t id;
+    int len;
+    bool tok_ok;
+    tile_lookup<SB, G>(slots, mask, s_tok, T, t0, max_n, id, len, tok_ok);
+    const int64_t t = t0 + threadIdx.x / G;
+    if (threadIdx.x % G == 0 && t < T) {
+        if (!tok_ok) atomicOr(err, err_bit(SCONE_ETOKEN));
+        if (ids_out) ids_out[b * T + t] = id;
+        if (len_out) len_out[b * T + t] = (int8_t)len;
     }
 }
 
@@ -70,11 +41,11 @@ template <int SB, int G>
 hipError_t launch(const scone_table* tb, const int32_t* X, int64_t B, int64_t T, int max_n,
                   int32_t* ids, int8_t* lens, unsigned* err, hipStream_t st) {
     using Slot = typename SlotOps<SB>::Slot;
-    constexpr int kTile = kLookupThreads / G;
-    const int64_t tiles = (T + kTile - 1) / kTile;
+    constexpr int P = TileShape<G>::kPositions;
+    const int64_t tiles = (T + P - 1) / P;
     const int64_t grid = B * tiles;
     if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((k_lookup<SB, G>), dim3((unsigned)grid), dim3(kLookupThreads), 0, st,
+    hipLaunchKernelGGL((k_lookup<SB, G>), dim3((unsigned)grid), dim3(kTileThreads), 0, st,
                        static_cast<const Slot*>(tb->slots), (uint64_t)tb->capacity - 1, X, T,
                        max_n, tiles, ids, lens, err);
     return hipGetLastError();
@@ -84,14 +55,22 @@ template <int SB>
 hipError_t dispatch_groups(const scone_table* tb, const int32_t* X, int64_t B, int64_t T,
                            int max_n, int32_t* ids, int8_t* lens, unsigned* err,
                            hipStream_t st) {
-    const int probes = max_n - 1;
-    if (probes <= 1) return launch<SB, 1>(tb, X, B, T, max_n, ids, lens, err, st);
-    if (probes <= 2) return launch<SB, 2>(tb, X, B, T, max_n, ids, lens, err, st);
-    if (probes <= 4) return launch<SB, 4>(tb, X, B, T, max_n, ids, lens, err, st);
-    return launch<SB, 8>(tb, X, B, T, max_n, ids, lens, err, st);
+    switch (lanes_for(max_n)) {
+        case 1: return launch<SB, 1>(tb, X, B, T, max_n, ids, lens, err, st);
+        case 2: return launch<SB, 2>(tb, X, B, T, max_n, ids, lens, err, st);
+        case 4: return launch<SB, 4>(tb, X, B, T, max_n, ids, lens, err, st);
+        default: return launch<SB, 8>(tb, X, B, T, max_n, ids, lens, err, st);
+    }
 }
 
 }  // namespace
+
+hipError_t launch_lookup(const scone_table* tb, const int32_t* X, int64_t B, int64_t T,
+                         int max_n, int32_t* ids, int8_t* lens, unsigned* err, hipStream_t st) {
+    return tb->slot_bytes == 16 ? dispatch_groups<16>(tb, X, B, T, max_n, ids, lens, err, st)
+                                : dispatch_groups<32>(tb, X, B, T, max_n, ids, lens, err, st);
+}
+
 }  // namespace scone
 
 extern "C" int scone_lookup(const scone_table_t* table, const int32_t* token_ids, int64_t B,
@@ -109,10 +88,7 @@ extern "C" int scone_lookup(const scone_table_t* table, const int32_t* token_ids
     if (!err) return SCONE_EHIP;
     const int eff = max_n < table->max_len ? max_n : table->max_len;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    const hipError_t e =
-        table->slot_bytes == 16
-            ? dispatch_groups<16>(table, token_ids, B, T, eff, fgram_ids, match_len, err, st)
-            : dispatch_groups<32>(table, token_ids, B, T, eff, fgram_ids, match_len, err, st);
+    const hipError_t e = launch_lookup(table, token_ids, B, T, eff, fgram_ids, match_len, err, st);
     if (e == hipErrorInvalidConfiguration) return SCONE_EINVAL;
     return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
 }

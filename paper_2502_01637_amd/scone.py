@@ -43,6 +43,10 @@ def _declare(L):
     L.scone_lookup.restype = I
     L.scone_gather.argtypes = [P, I64, P, I64, I64, P, I32, P]
     L.scone_gather.restype = I
+    L.scone_embed.argtypes = [P, P, I64, I64, I32, P, I64, I64, I32, P, P, P, P]
+    L.scone_embed.restype = I
+    L.scone_decode_step.argtypes = [P, P, P, I32, P, I64, I32, P, I64, I64, I32, P, P, P, P]
+    L.scone_decode_step.restype = I
     L.scone_host_alloc.argtypes = [I64, ctypes.POINTER(P), ctypes.POINTER(P)]
     L.scone_host_alloc.restype = I
     L.scone_host_free.argtypes = [P]
@@ -215,18 +219,7 @@ def gather(fgram_ids: torch.Tensor, rows, out: Optional[torch.Tensor] = None,
     """scone_gather: out[k] = rows[fgram_ids[k]]; rows is a CUDA tensor or HostRows."""
     _dev_i32(fgram_ids, "fgram_ids")
     n_tok = fgram_ids.numel()
-    if isinstance(rows, HostRows):
-        placement, base = PLACE_HOST, rows.device_ptr
-        n_rows, row_bytes, row_shape, dtype = rows.n_rows, rows.row_bytes, rows.row_shape, rows.dtype
-    else:
-        if not isinstance(rows, torch.Tensor) or rows.device.type != "cuda":
-            raise TypeError("rows must be a CUDA tensor or HostRows")
-        if not rows.is_contiguous() or rows.dim() < 1:
-            raise ValueError("rows must be a contiguous [n_rows, ...] tensor")
-        placement, base = PLACE_HBM, _ptr(rows)
-        n_rows, row_shape, dtype = rows.shape[0], tuple(rows.shape[1:]), rows.dtype
-        row_bytes = rows[0].numel() * rows.element_size() if n_rows else \
-            int(torch.Size(row_shape).numel()) * rows.element_size()
+    placement, base, n_rows, row_bytes, row_shape, dtype = _rows_arg(rows)
     if out is None:
         out = torch.empty(tuple(fgram_ids.shape) + row_shape, dtype=dtype,
                           device=fgram_ids.device)
@@ -236,6 +229,66 @@ def gather(fgram_ids: torch.Tensor, rows, out: Optional[torch.Tensor] = None,
         rc = lib().scone_gather(_ptr(fgram_ids), n_tok, base, n_rows, row_bytes, _ptr(out),
                                 placement, _stream(stream))
     _check(rc, "scone_gather")
+    return out
+
+
+def _rows_arg(rows):
+    """(placement, pointer, n_rows, row_bytes, row_shape, dtype) of a row table."""
+    if isinstance(rows, HostRows):
+        return PLACE_HOST, rows.device_ptr, rows.n_rows, rows.row_bytes, rows.row_shape, rows.dtype
+    if not isinstance(rows, torch.Tensor) or rows.device.type != "cuda":
+        raise TypeError("rows must be a CUDA tensor or HostRows")
+    if not rows.is_contiguous() or rows.dim() < 1:
+        raise ValueError("rows must be a contiguous [n_rows, ...] tensor")
+    row_shape = tuple(rows.shape[1:])
+    row_bytes = int(torch.Size(row_shape).numel()) * rows.element_size()
+    return PLACE_HBM, _ptr(rows), rows.shape[0], row_bytes, row_shape, rows.dtype
+
+
+def embed(table: Table, token_ids: torch.Tensor, max_n: int, rows, out=None,
+          fgram_ids: Optional[torch.Tensor] = None, match_len: Optional[torch.Tensor] = None,
+          stream=None) -> torch.Tensor:
+    """scone_embed: fused lookup + gather; returns out [B, T, *row_shape]."""
+    _dev_i32(token_ids, "token_ids", 2)
+    B, T = token_ids.shape
+    placement, base, n_rows, row_bytes, row_shape, dtype = _rows_arg(rows)
+    if out is None:
+        out = torch.empty((B, T) + row_shape, dtype=dtype, device=token_ids.device)
+    if not out.is_contiguous() or out.numel() * out.element_size() != B * T * row_bytes:
+        raise ValueError("out must be contiguous with B * T * row_bytes bytes")
+    for name, t, dt in (("fgram_ids", fgram_ids, torch.int32), ("match_len", match_len, torch.int8)):
+        if t is not None and (t.dtype != dt or t.numel() != B * T or not t.is_contiguous()
+                              or t.device != token_ids.device):
+            raise ValueError(f"{name} must be a contiguous {dt} device tensor of B*T elements")
+    with torch.cuda.device(token_ids.device):
+        rc = lib().scone_embed(table.handle, _ptr(token_ids), B, T, int(max_n), base, n_rows,
+                               row_bytes, placement, _ptr(out), _ptr(fgram_ids), _ptr(match_len),
+                               _stream(stream))
+    _check(rc, "scone_embed")
+    return out
+
+
+def decode_step(table: Table, ctx: torch.Tensor, ctx_len: torch.Tensor, new_tok: torch.Tensor,
+                max_n: int, rows, out: torch.Tensor, fgram_ids: Optional[torch.Tensor] = None,
+                match_len: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """scone_decode_step: ctx [S, cap] and ctx_len [S] are updated in place."""
+    _dev_i32(ctx, "ctx", 2)
+    _dev_i32(ctx_len, "ctx_len", 1)
+    _dev_i32(new_tok, "new_tok", 1)
+    S, cap = ctx.shape
+    if ctx_len.numel() != S or new_tok.numel() != S:
+        raise ValueError("ctx, ctx_len and new_tok disagree on S")
+    placement, base, n_rows, row_bytes, _, _ = _rows_arg(rows)
+    if not out.is_contiguous() or out.numel() * out.element_size() != S * row_bytes:
+        raise ValueError("out must be contiguous with S * row_bytes bytes")
+    for name, t, dt in (("fgram_ids", fgram_ids, torch.int32), ("match_len", match_len, torch.int8)):
+        if t is not None and (t.dtype != dt or t.numel() != S or not t.is_contiguous()):
+            raise ValueError(f"{name} must be a contiguous {dt} tensor of S elements")
+    with torch.cuda.device(ctx.device):
+        rc = lib().scone_decode_step(table.handle, _ptr(ctx), _ptr(ctx_len), cap, _ptr(new_tok),
+                                     S, int(max_n), base, n_rows, row_bytes, placement, _ptr(out),
+                                     _ptr(fgram_ids), _ptr(match_len), _stream(stream))
+    _check(rc, "scone_decode_step")
     return out
 
 

@@ -230,3 +230,120 @@ def test_lookup_and_gather_errors_raise_through_check():
     S.gather(dev(np.array([0], dtype=np.int32)), empty_rows)
     assert S.check() == S.scone.EROW
     raises_code(S.scone.EINVAL, S.lookup, tb, X, 0)
+
+
+# ------------------------------------------------------- fused and decode --
+
+@pytest.mark.parametrize("case", ["tiny", "c2_small", "c3_small", "k7_small", "odd_rows"])
+@pytest.mark.parametrize("outputs", [True, False])
+def test_embed_matches_oracle(case, outputs):
+    if case == "tiny":
+        cfg = CONFIGS["tiny"]
+    elif case == "c2_small":
+        cfg = scaled(CONFIGS["c2_1m"], n_fgrams=20_000, B=3, T=1500)
+    elif case == "c3_small":
+        cfg = scaled(CONFIGS["c3_10m_k5"], n_fgrams=40_000, B=2, T=2100, d=512)
+    elif case == "k7_small":
+        cfg = scaled(CONFIGS["tiny"], V=40, n_fgrams=3000, max_len=7, max_n=7, B=3, T=700, d=24)
+    else:
+        cfg = scaled(CONFIGS["tiny"], d=7, B=5, T=333)  # 28-byte rows: byte path
+    w = make_workload(cfg)
+    o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+    exp_ids, exp_len = o.lookup(w.tokens, cfg.max_n)
+    E = device_rows(cfg)
+    tb = build_gpu(w.fgrams, w.lengths, w.ids)
+    ids = torch.empty((cfg.B, cfg.T), dtype=torch.int32, device="cuda") if outputs else None
+    ml = torch.empty((cfg.B, cfg.T), dtype=torch.int8, device="cuda") if outputs else None
+    out = S.embed(tb, dev(w.tokens), cfg.max_n, E, fgram_ids=ids, match_len=ml)
+    S.check_ok()
+    exp = oracle.gather(exp_ids, E.cpu().view(torch.uint8).numpy())
+    assert as_bytes(out).tobytes() == exp.tobytes()
+    if outputs:
+        np.testing.assert_array_equal(ids.cpu().numpy(), exp_ids)
+        np.testing.assert_array_equal(ml.cpu().numpy(), exp_len)
+
+
+def test_embed_errors_and_rowless_table():
+    tb = build_gpu(pad([[1, 2]], 3), [2], [10])
+    E = torch.arange(12 * 8, dtype=torch.float32, device="cuda").view(12, 8)
+    X = dev(np.array([[1, 2, 11, 3]], dtype=np.int32))
+    out = S.embed(tb, X, 3, E)
+    S.check_ok()
+    assert torch.equal(out[0, 1], E[10]) and torch.equal(out[0, 2], E[11])
+    small = E[:5].contiguous()          # ids 10 and 11 fall outside
+    ids = torch.empty((1, 4), dtype=torch.int32, device="cuda")
+    out = S.embed(tb, X, 3, small, fgram_ids=ids)
+    assert S.check() == S.scone.EROW
+    assert ids.cpu().tolist() == [[1, 10, 11, 3]]
+    assert (out[0, 1] == 0).all() and torch.equal(out[0, 0], small[1])
+    S.embed(tb, dev(np.array([[1, 70000]], dtype=np.int32)), 3, E)
+    assert S.check() == S.scone.ETOKEN
+    out = S.embed(tb, X, 3, E[:0], fgram_ids=ids)
+    assert S.check() == S.scone.EROW
+    assert ids.cpu().tolist() == [[1, 10, 11, 3]] and (out == 0).all()
+
+
+def decode_all(tb, X, max_n, E, cap, host=None):
+    """Feed X[:, s] step by step; returns per-step ids, lens and rows."""
+    Sq, steps = X.shape
+    Xd = dev(X)
+    ctx = torch.full((Sq, cap), -7, dtype=torch.int32, device="cuda")
+    clen = torch.zeros(Sq, dtype=torch.int32, device="cuda")
+    rows = E if host is None else host
+    ids, lens, outs = [], [], []
+    for s in range(steps):
+        i = torch.empty(Sq, dtype=torch.int32, device="cuda")
+        m = torch.empty(Sq, dtype=torch.int8, device="cuda")
+        o = torch.empty((Sq, E.shape[1]), dtype=E.dtype, device="cuda")
+        S.decode_step(tb, ctx, clen, Xd[:, s].contiguous(), max_n, rows, o, fgram_ids=i,
+                      match_len=m)
+        ids.append(i)
+        lens.append(m)
+        outs.append(o)
+    S.check_ok()
+    return (torch.stack(ids, 1).cpu().numpy(), torch.stack(lens, 1).cpu().numpy(),
+            torch.stack(outs, 1))
+
+
+@pytest.mark.parametrize("max_len,max_n,cap", [(3, 3, 2), (3, 3, 6), (5, 5, 4), (7, 7, 6),
+                                               (3, 1, 0), (3, 9, 2)])
+def test_decode_equals_prefill(max_len, max_n, cap):
+    cfg = scaled(CONFIGS["c5_decode"], V=50 if max_len > 3 else 32768,
+                 n_fgrams=4000 if max_len > 3 else 20_000, max_len=max_len, max_n=max_n, B=37,
+                 T=40, d=64)
+    w = make_workload(cfg)
+    o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+    exp_ids, exp_len = o.lookup(w.tokens, max_n)
+    E = device_rows(cfg)
+    tb = build_gpu(w.fgrams, w.lengths, w.ids)
+    ids, lens, outs = decode_all(tb, w.tokens, max_n, E, cap)
+    np.testing.assert_array_equal(ids, exp_ids)
+    np.testing.assert_array_equal(lens, exp_len)
+    exp = oracle.gather(exp_ids, E.cpu().view(torch.uint8).numpy())
+    assert as_bytes(outs).tobytes() == exp.tobytes()
+
+
+def test_decode_host_rows_and_errors():
+    cfg = scaled(CONFIGS["c5_decode"], n_fgrams=5000, B=16, T=12, d=128)
+    w = make_workload(cfg)
+    o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+    exp_ids, _ = o.lookup(w.tokens, 3)
+    tb = build_gpu(w.fgrams, w.lengths, w.ids)
+    host = S.HostRows(cfg.n_rows, (cfg.d,), torch.bfloat16)
+    try:
+        host.tensor().copy_(table_rows(cfg, range(cfg.n_rows)))
+        E = torch.empty((1, cfg.d), dtype=torch.bfloat16, device="cuda")  # shape carrier only
+        ids, _, outs = decode_all(tb, w.tokens, 3, E, 2, host=host)
+        np.testing.assert_array_equal(ids, exp_ids)
+        exp = oracle.gather(exp_ids, host.tensor().view(torch.uint8).numpy())
+        assert as_bytes(outs).tobytes() == exp.tobytes()
+    finally:
+        host.close()
+    ctx = torch.zeros((2, 2), dtype=torch.int32, device="cuda")
+    clen = torch.zeros(2, dtype=torch.int32, device="cuda")
+    out = torch.empty((2, 4), dtype=torch.float32, device="cuda")
+    rows = torch.zeros((10, 4), dtype=torch.float32, device="cuda")
+    raises_code(S.scone.EINVAL, S.decode_step, tb, ctx[:, :1].contiguous(), clen,
+                dev(np.array([1, 2], np.int32)), 3, rows, out)  # context too short for max_n 3
+    S.decode_step(tb, ctx, clen, dev(np.array([1, 70000], np.int32)), 3, rows, out)
+    assert S.check() == S.scone.ETOKEN  # also EROW: token 70000 is not a row; lowest code wins
