@@ -3,36 +3,71 @@
 // Each workgroup first resolves the longest match for its tile of positions
 // (the same tile lookup as scone_lookup, ids kept in LDS), then copies the
 // tile's rows into the contiguous output block that those positions own.
-// Fusing removes the id round trip through HBM and, more importantly, the
-// separate latency-bound lookup launch: while some workgroups wait on hash
-// probes, the others on the same compute unit keep HBM busy with row copies.
+// Fusing removes the id round trip through HBM and the separate
+// latency-bound lookup launch.  Tiles are small (about 64 KiB of rows) so the
+// grid holds several generations of workgroups: once the first generation
+// staggers, some workgroups wait on hash probes while the others on the same
+// compute unit keep HBM busy with row copies.
 #include "tile_lookup.h"
 
 namespace scone {
 namespace {
 
+// Row copy helpers for one batch of U units per thread (unit i of the tile's
+// output block).  A bad id reads row 0 and the unit is zeroed afterwards, so
+// the loads of a batch carry no branch and stay in flight together.
+template <typename V, int U, bool kPow2>
+struct TileCopy {
+    const int32_t* s_id;
+    const V* __restrict__ rows;
+    V* __restrict__ dst;
+    int64_t n_rows, upr;
+    int shift;
+
+    __device__ __forceinline__ void load(int64_t base, V (&v)[U], bool (&ok)[U]) const {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t i = base + (int64_t)u * kTileThreads;
+            const int64_t r = kPow2 ? (i >> shift) : (i / upr);
+            const int64_t c = i - r * upr;
+            const int64_t id = s_id[r];
+            ok[u] = (id >= 0) & (id < n_rows);
+            const int64_t src = ok[u] ? id : 0;
+            v[u] = rows[(kPow2 ? (src << shift) : src * upr) + c];
+        }
+    }
+    __device__ __forceinline__ bool store(int64_t base, V (&v)[U], const bool (&ok)[U]) const {
+        bool bad = false;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            __builtin_nontemporal_store(ok[u] ? v[u] : V{}, dst + base + (int64_t)u * kTileThreads);
+            bad |= !ok[u];
+        }
+        return bad;
+    }
+};
+
 template <int SB, int G, typename V, int U, bool kPow2>
 __global__ __launch_bounds__(kTileThreads) void k_embed(
     const typename SlotOps<SB>::Slot* __restrict__ slots, uint64_t mask,
-    const int32_t* __restrict__ X, int64_t T, int max_n, int64_t tiles_per_row,
+    const int32_t* __restrict__ X, int64_t T, int P, int max_n, int64_t tiles_per_row,
     const V* __restrict__ rows, int64_t n_rows, int64_t upr, int shift, V* __restrict__ out,
     int32_t* __restrict__ ids_out, int8_t* __restrict__ len_out, unsigned* __restrict__ err) {
-    constexpr int P = TileShape<G>::kPositions;
-    __shared__ int32_t s_tok[P + kMaxHalo];
-    __shared__ int32_t s_id[P];
+    __shared__ int32_t s_tok[TileShape<G>::kPositions + kMaxHalo];
+    __shared__ int32_t s_id[TileShape<G>::kPositions];
 
     const int64_t b = blockIdx.x / tiles_per_row;
     const int64_t t0 = (blockIdx.x - b * tiles_per_row) * (int64_t)P;
-    stage_tokens<G>(s_tok, X + b * T, T, t0, max_n - 1);
+    stage_tokens(s_tok, X + b * T, T, t0, P, max_n - 1);
     __syncthreads();
-    {
+    if (threadIdx.x < ((P * G + 63) & ~63)) {  // whole waves only
         int32_t id;
         int len;
         bool tok_ok;
-        tile_lookup<SB, G>(slots, mask, s_tok, T, t0, max_n, id, len, tok_ok);
+        tile_lookup<SB, G>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok);
         const int p = threadIdx.x / G;
         const int64_t t = t0 + p;
-        if (threadIdx.x % G == 0) {
+        if (threadIdx.x % G == 0 && p < P) {
             s_id[p] = id;
             if (t < T) {
                 if (!tok_ok) atomicOr(err, err_bit(SCONE_ETOKEN));
@@ -44,46 +79,40 @@ __global__ __launch_bounds__(kTileThreads) void k_embed(
     __syncthreads();
 
     // Copy the tile's rows: positions t0 .. t0+npos-1 own one contiguous
-    // output block of npos * upr units.
+    // output block of npos * upr units.  Whole batches are software-pipelined
+    // (the next batch's loads are issued before this batch's stores).
     const int64_t npos = (T - t0) < P ? (T - t0) : P;
     const int64_t total = npos * upr;
-    V* __restrict__ dst = out + (b * T + t0) * upr;
+    const TileCopy<V, U, kPow2> cp{s_id, rows, out + (b * T + t0) * upr, n_rows, upr, shift};
+    constexpr int64_t kStride = (int64_t)kTileThreads * U;
+    const int64_t whole = total / kStride * kStride;
     bool bad = false;
-    for (int64_t base = threadIdx.x; base < total; base += (int64_t)kTileThreads * U) {
-        V v[U];
-        bool ok[U];
-        if (base + (int64_t)(U - 1) * kTileThreads < total) {
+    int64_t base = threadIdx.x;
+    if (whole > 0) {
+        V a[U];
+        bool oka[U];
+        cp.load(base, a, oka);
+        for (; base + kStride < whole; base += kStride) {
+            V nb[U];
+            bool okb[U];
+            cp.load(base + kStride, nb, okb);
+            bad |= cp.store(base, a, oka);
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int64_t i = base + (int64_t)u * kTileThreads;
-                const int64_t r = kPow2 ? (i >> shift) : (i / upr);
-                const int64_t c = i - r * upr;
-                const int64_t id = s_id[r];
-                ok[u] = (id >= 0) & (id < n_rows);
-                const int64_t src = ok[u] ? id : 0;
-                v[u] = rows[(kPow2 ? (src << shift) : src * upr) + c];
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                if (!ok[u]) v[u] = V{};
-                __builtin_nontemporal_store(v[u], dst + base + (int64_t)u * kTileThreads);
-                bad |= !ok[u];
-            }
-        } else {
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int64_t i = base + (int64_t)u * kTileThreads;
-                if (i < total) {
-                    const int64_t r = kPow2 ? (i >> shift) : (i / upr);
-                    const int64_t c = i - r * upr;
-                    const int64_t id = s_id[r];
-                    const bool okk = (id >= 0) & (id < n_rows);
-                    const V val = okk ? rows[id * upr + c] : V{};
-                    __builtin_nontemporal_store(val, dst + i);
-                    bad |= !okk;
-                }
+                a[u] = nb[u];
+                oka[u] = okb[u];
             }
         }
+        bad |= cp.store(base, a, oka);
+        base += kStride;
+    }
+    for (int64_t i = base; i < total; i += kTileThreads) {  // ragged remainder
+        const int64_t r = kPow2 ? (i >> shift) : (i / upr);
+        const int64_t c = i - r * upr;
+        const int64_t id = s_id[r];
+        const bool okk = (id >= 0) & (id < n_rows);
+        __builtin_nontemporal_store(okk ? rows[id * upr + c] : V{}, cp.dst + i);
+        bad |= !okk;
     }
     if (bad) atomicOr(err, err_bit(SCONE_EROW));
 }
@@ -93,13 +122,17 @@ hipError_t launch(const scone_table* tb, const int32_t* X, int64_t B, int64_t T,
                   const void* rows, int64_t n_rows, int64_t upr, int shift, void* out,
                   int32_t* ids, int8_t* lens, unsigned* err, hipStream_t st) {
     using Slot = typename SlotOps<SB>::Slot;
-    constexpr int P = TileShape<G>::kPositions;
+    // Positions per workgroup: about 64 KiB of rows, so that many short-lived
+    // workgroups overlap one another's probes with their copies.
+    const int64_t row_bytes = upr * (int64_t)sizeof(V);
+    int P = TileShape<G>::kPositions;
+    while (P > 1 && (int64_t)P * row_bytes > (64 << 10)) P >>= 1;
     const int64_t tiles = (T + P - 1) / P;
     const int64_t grid = B * tiles;
     if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL((k_embed<SB, G, V, 4, kPow2>), dim3((unsigned)grid), dim3(kTileThreads),
                        0, st, static_cast<const Slot*>(tb->slots), (uint64_t)tb->capacity - 1, X,
-                       T, max_n, tiles, static_cast<const V*>(rows), n_rows, upr, shift,
+                       T, P, max_n, tiles, static_cast<const V*>(rows), n_rows, upr, shift,
                        static_cast<V*>(out), ids, lens, err);
     return hipGetLastError();
 }

@@ -23,12 +23,12 @@ __global__ __launch_bounds__(kTileThreads) void k_lookup(
     __shared__ int32_t s_tok[P + kMaxHalo];
     const int64_t b = blockIdx.x / tiles_per_row;
     const int64_t t0 = (blockIdx.x - b * tiles_per_row) * (int64_t)P;
-    stage_tokens<G>(s_tok, X + b * T, T, t0, max_n - 1);
+    stage_tokens(s_tok, X + b * T, T, t0, P, max_n - 1);
     __syncthreads();
     int32_t id;
     int len;
     bool tok_ok;
-    tile_lookup<SB, G>(slots, mask, s_tok, T, t0, max_n, id, len, tok_ok);
+    tile_lookup<SB, G>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok);
     const int64_t t = t0 + threadIdx.x / G;
     if (threadIdx.x % G == 0 && t < T) {
         if (!tok_ok) atomicOr(err, err_bit(SCONE_ETOKEN));

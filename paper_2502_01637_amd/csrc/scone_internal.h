@@ -132,22 +132,44 @@ struct SlotOps<32> {
     }
 };
 
-// Linear probe from the key's home slot.  Returns true and the id on a hit;
-// false when an empty slot is reached first.  Bounded by the slot count.
+// Probing is linear, slot by slot, but starts at the first slot of the
+// key's 64-byte bucket (the aligned group of 64 / SB slots that holds its
+// hash slot).  Insertion claims the first empty slot in that order, so a
+// lookup can read a whole bucket at once: a match anywhere in it is the key,
+// and an empty slot in it (with no match) means the key is absent, because
+// nothing is ever removed.  One round of independent loads usually settles
+// a probe, instead of a chain of dependent single-slot loads.
+template <int SB>
+struct Bucket {
+    static constexpr int kSlots = 64 / SB;
+};
+
+__device__ __forceinline__ uint64_t home_slot(const Key& k, uint64_t mask, int bucket_slots) {
+    return (hash_key(k) & mask) & ~(uint64_t)(bucket_slots - 1);
+}
+
+// Returns true and the id on a hit.  Bounded by the slot count.
 template <int SB>
 __device__ __forceinline__ bool probe(const typename SlotOps<SB>::Slot* slots, uint64_t mask,
                                       const Key& k, int32_t& id_out) {
-    uint64_t s = hash_key(k) & mask;
-    for (uint64_t step = 0; step <= mask; ++step) {
-        uint64_t w0, w1;
-        int32_t id;
-        SlotOps<SB>::read(slots, s, w0, w1, id);
-        if (w0 == k.w0 && w1 == k.w1) {
-            id_out = id;
-            return true;
+    constexpr int BW = Bucket<SB>::kSlots;
+    uint64_t s = home_slot(k, mask, BW);
+    for (uint64_t step = 0; step <= mask; step += BW) {
+        uint64_t w0[BW], w1[BW];
+        int32_t id[BW];
+#pragma unroll
+        for (int i = 0; i < BW; ++i) SlotOps<SB>::read(slots, s + i, w0[i], w1[i], id[i]);
+        bool empty = false;
+#pragma unroll
+        for (int i = 0; i < BW; ++i) {
+            if (w0[i] == k.w0 && w1[i] == k.w1) {
+                id_out = id[i];
+                return true;
+            }
+            empty |= w0[i] == 0;
         }
-        if (w0 == 0) return false;
-        s = (s + 1) & mask;
+        if (empty) return false;
+        s = (s + BW) & mask;
     }
     return false;
 }

@@ -3,8 +3,9 @@
 // The paper stores the f-gram layer as a dense row matrix plus a hash
 // dictionary from f-grams to row indices (Section 2), built before serving
 // (Section 3.2).  Here the dictionary is a power-of-two array of slots with
-// linear probing.  Insertion claims the first empty slot on the key's probe
-// path with a 64-bit compare-and-swap on the slot's first key word, then
+// linear probing from the start of the key's 64-byte bucket.  Insertion
+// claims the first empty slot on the key's probe path with a 64-bit
+// compare-and-swap on the slot's first key word, then
 // writes the rest of the key and the id; it never compares keys, so slot
 // placement under concurrency does not matter.  A second pass re-probes every
 // input key: the first slot holding that key must be the one its own thread
@@ -51,7 +52,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_insert(
         return;
     }
     const Key key = pack_key(tok, len);
-    uint64_t s = hash_key(key) & mask;
+    uint64_t s = home_slot(key, mask, Bucket<SB>::kSlots);
     for (uint64_t step = 0; step <= mask; ++step) {
         unsigned long long* w0 = reinterpret_cast<unsigned long long*>(&slots[s].w0);
         if (atomicCAS(w0, 0ull, (unsigned long long)key.w0) == 0ull) {
@@ -74,7 +75,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_verify(
     const int64_t mine = slot_of[k];
     if (mine < 0) return;  // rejected or not placed: already reported
     const Key key = pack_key(fgrams + k * (int64_t)max_len, lengths[k]);
-    uint64_t s = hash_key(key) & mask;
+    uint64_t s = home_slot(key, mask, Bucket<SB>::kSlots);
     for (uint64_t step = 0; step <= mask; ++step) {
         uint64_t w0, w1;
         int32_t id;

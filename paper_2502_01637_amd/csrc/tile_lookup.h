@@ -10,7 +10,7 @@ constexpr int kMaxHalo = SCONE_MAX_FGRAM_LEN - 1;
 
 template <int G>
 struct TileShape {
-    static constexpr int kPositions = kTileThreads / G;  // positions per workgroup
+    static constexpr int kPositions = kTileThreads / G;  // most positions a workgroup can probe
 };
 
 // Lanes per position for a window of max_n: a power of two >= max_n - 1.
@@ -18,38 +18,37 @@ __host__ __device__ constexpr int lanes_for(int max_n) {
     return max_n - 1 <= 1 ? 1 : max_n - 1 <= 2 ? 2 : max_n - 1 <= 4 ? 4 : 8;
 }
 
-// Stage X[b, t0 - halo .. t0 + kPositions) of one row into LDS (zero outside
-// [0, T)); must be called by the whole workgroup, which then synchronises.
-template <int G>
+// Stage X[b, t0 - halo .. t0 + P) of one row into LDS (zero outside [0, T));
+// called by the whole workgroup, which then synchronises.
 __device__ __forceinline__ void stage_tokens(int32_t* s_tok, const int32_t* __restrict__ row,
-                                             int64_t T, int64_t t0, int halo) {
-    constexpr int P = TileShape<G>::kPositions;
+                                             int64_t T, int64_t t0, int P, int halo) {
     for (int i = threadIdx.x; i < P + halo; i += kTileThreads) {
         const int64_t t = t0 - halo + i;
         s_tok[i] = (t >= 0 && t < T) ? row[t] : 0;
     }
 }
 
-// After stage_tokens and a barrier: every position p = threadIdx.x / G of the
-// tile gets its longest match.  Lane j of the position's group probes the
-// suffix of length max_n - j; a wave ballot picks the lowest hitting lane
-// (the longest match) and a shuffle brings its id to lane j = 0.  Returns, on
-// lane j = 0 of a position inside the row, the id (or the token itself) and
-// the matched length (1 when nothing matched); `tok_ok` reports whether the
-// position's own token is in range.  All lanes of the wave must call it.
+// After stage_tokens and a barrier: position p = threadIdx.x / G (p < P) of
+// the tile gets its longest match.  Lane j of the position's group probes the
+// suffix of length max_n - j; a wave ballot picks the lowest hitting lane (the
+// longest match) and a shuffle brings its id to lane j = 0.  Returns, on lane
+// j = 0 of a valid position (p < P, t0 + p < T), the id (or the token itself)
+// and the matched length (1 when nothing matched); `tok_ok` reports whether
+// the position's own token is in range.  All lanes of the wave must call it.
 template <int SB, int G>
 __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __restrict__ slots,
                                             uint64_t mask, const int32_t* s_tok, int64_t T,
-                                            int64_t t0, int max_n, int32_t& id_out,
+                                            int64_t t0, int P, int max_n, int32_t& id_out,
                                             int& len_out, bool& tok_ok) {
     const int halo = max_n - 1;
     const int p = threadIdx.x / G;
     const int j = threadIdx.x % G;
     const int64_t t = t0 + p;
+    const bool valid = p < P && t < T;
     const int n = max_n - j;
     bool hit = false;
     int32_t id = 0;
-    if (t < T && n >= 2 && (int64_t)n <= t + 1) {
+    if (valid && n >= 2 && (int64_t)n <= t + 1) {
         const int32_t* win = s_tok + p + halo - n + 1;  // X[b, t-n+1 .. t]
         bool ok = true;
 #pragma unroll
@@ -63,7 +62,7 @@ __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __
     const unsigned gm = (unsigned)(m >> base) & ((1u << G) - 1u);
     const int jb = gm ? __ffs(gm) - 1 : 0;
     const int32_t best = __shfl(id, base + jb);
-    const int32_t tok = s_tok[p + halo];
+    const int32_t tok = valid ? s_tok[p + halo] : 0;
     tok_ok = (tok >= 0) & (tok < SCONE_TOKEN_LIMIT);
     id_out = gm ? best : tok;
     len_out = gm ? max_n - jb : 1;
