@@ -1,9 +1,10 @@
 // Row gather: out[k, :] = rows[ids[k], :] as raw bytes.
 //
 // The embedding fetch is a pure memory copy (Section 1), so the kernel is an
-// HBM-bound streaming copy whose source rows are chosen by the ids.  The
-// output is viewed as a flat array of V-sized units (16 bytes when the row
-// width and the pointers allow).  Consecutive lanes own consecutive units, so
+// HBM-bound streaming copy whose source rows are chosen by the ids.  Rows of
+// 1, 2, 4 or 8 KiB (16-byte aligned) take one wavefront per row.  Any other
+// width views the output as a flat array of V-sized units (16 bytes when the
+// row width and the pointers allow).  Consecutive lanes own consecutive units, so
 // one wavefront reads 64 * 16 B = 1 KiB of one row per instruction and writes
 // the same 1 KiB of the output; each thread issues all of its U loads before
 // its U stores to keep enough bytes in flight.  Output stores are
@@ -71,6 +72,29 @@ __global__ __launch_bounds__(kGatherThreads) void k_gather(
     if (bad) atomicOr(err, err_bit(SCONE_EROW));
 }
 
+// Rows of 64*U 16-byte units (1, 2, 4 or 8 KiB): one wavefront per row, four
+// rows per workgroup.  The row id is wave-uniform, so it is read once into a
+// scalar register and every load is a scalar row base plus the lane offset.
+template <int U>
+__global__ __launch_bounds__(kGatherThreads) void k_gather_rows(
+    const int32_t* __restrict__ ids, int64_t n_tok, const u32x4* __restrict__ rows,
+    int64_t n_rows, u32x4* __restrict__ out, unsigned* __restrict__ err) {
+    const int64_t r = (int64_t)blockIdx.x * (kGatherThreads / 64) +
+                      __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (r >= n_tok) return;  // wave-uniform
+    const int lane = threadIdx.x & 63;
+    const int64_t id = ids[r];
+    const bool ok = (id >= 0) & (id < n_rows);
+    const u32x4* src = rows + (ok ? id : 0) * (64 * U);
+    u32x4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = src[u * 64 + lane];
+    u32x4* dst = out + r * (64 * U);
+#pragma unroll
+    for (int u = 0; u < U; ++u) __builtin_nontemporal_store(ok ? v[u] : u32x4{}, dst + u * 64 + lane);
+    if (!ok && lane == 0) atomicOr(err, err_bit(SCONE_EROW));
+}
+
 // Every id is out of range when the table has no rows: zero the output.
 template <typename V>
 __global__ __launch_bounds__(kGatherThreads) void k_zero(int64_t total, V* __restrict__ out,
@@ -135,7 +159,21 @@ extern "C" int scone_gather(const int32_t* fgram_ids, int64_t n_tok, const void*
     // Widest unit that divides the row width and both base addresses.
     const uintptr_t align = (uintptr_t)rows | (uintptr_t)out | (uintptr_t)row_bytes;
     hipError_t e;
-    if ((align & 15) == 0)
+    const int64_t upr16 = row_bytes / 16;
+    if ((align & 15) == 0 && n_rows > 0 &&
+        (upr16 == 64 || upr16 == 128 || upr16 == 256 || upr16 == 512)) {
+        const int64_t grid = (n_tok + kGatherThreads / 64 - 1) / (kGatherThreads / 64);
+        if (grid > 0x7fffffffLL) return SCONE_EINVAL;
+        const u32x4* R = static_cast<const u32x4*>(rows);
+        u32x4* O = static_cast<u32x4*>(out);
+        switch (upr16) {
+            case 64: hipLaunchKernelGGL(k_gather_rows<1>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, fgram_ids, n_tok, R, n_rows, O, err); break;
+            case 128: hipLaunchKernelGGL(k_gather_rows<2>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, fgram_ids, n_tok, R, n_rows, O, err); break;
+            case 256: hipLaunchKernelGGL(k_gather_rows<4>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, fgram_ids, n_tok, R, n_rows, O, err); break;
+            default: hipLaunchKernelGGL(k_gather_rows<8>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, fgram_ids, n_tok, R, n_rows, O, err); break;
+        }
+        e = hipGetLastError();
+    } else if ((align & 15) == 0)
         e = launch_gather<u32x4, 4>(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err, st);
     else if ((align & 7) == 0)
         e = launch_gather<u32x2, 4>(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err, st);

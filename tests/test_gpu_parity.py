@@ -137,7 +137,8 @@ def test_empty_inputs():
     assert out.shape == (0, 8)
 
 
-@pytest.mark.parametrize("row_bytes", [1, 2, 3, 6, 12, 16, 48, 256, 2048, 4096, 4100])
+@pytest.mark.parametrize("row_bytes", [1, 2, 3, 6, 12, 16, 48, 256, 1024, 2048, 4096, 4100,
+                                       8192])
 @pytest.mark.parametrize("offset", [0, 1, 4])
 def test_gather_row_widths_and_alignment(row_bytes, offset):
     rng = np.random.default_rng(row_bytes + offset)
@@ -226,6 +227,13 @@ def test_lookup_and_gather_errors_raise_through_check():
     got = out.cpu()
     assert torch.equal(got[0], E[1].cpu()) and torch.equal(got[2], E[3].cpu())
     assert (got[1] == 0).all() and (got[3] == 0).all()
+    # the same through the one-wavefront-per-row path (2 KiB rows)
+    Eb = torch.arange(8 * 1024, dtype=torch.int16, device="cuda").view(8, 1024).to(torch.bfloat16)
+    out = S.gather(dev(np.array([7, 8, 0, -3, 2], dtype=np.int32)), Eb)
+    assert S.check() == S.scone.EROW
+    got = out.cpu()
+    assert torch.equal(got[0], Eb[7].cpu()) and torch.equal(got[2], Eb[0].cpu())
+    assert (got[1].view(torch.int16) == 0).all() and (got[3].view(torch.int16) == 0).all()
     empty_rows = torch.zeros((0, 4), dtype=torch.float32, device="cuda")
     S.gather(dev(np.array([0], dtype=np.int32)), empty_rows)
     assert S.check() == S.scone.EROW
@@ -347,3 +355,38 @@ def test_decode_host_rows_and_errors():
                 dev(np.array([1, 2], np.int32)), 3, rows, out)  # context too short for max_n 3
     S.decode_step(tb, ctx, clen, dev(np.array([1, 70000], np.int32)), 3, rows, out)
     assert S.check() == S.scone.ETOKEN  # also EROW: token 70000 is not a row; lowest code wins
+
+
+@pytest.mark.parametrize("max_len,max_n,d,T", [(3, 3, 1024, 8190), (5, 5, 2048, 4099),
+                                               (3, 2, 1024, 8192), (7, 7, 512, 8191),
+                                               (7, 6, 2048, 2053), (3, 3, 64, 9000)])
+def test_embed_many_tiles_per_workgroup(max_len, max_n, d, T):
+    # enough tiles that each resident workgroup walks several of them, with a
+    # ragged last tile in most rows
+    V = 32768 if max_len <= 5 else 60
+    cfg = scaled(CONFIGS["c2_1m"], V=V, n_fgrams=30_000, max_len=max_len, max_n=max_n, d=d,
+                 B=8, T=T)
+    w = make_workload(cfg)
+    o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+    exp_ids, exp_len = o.lookup(w.tokens, max_n)
+    E = device_rows(cfg)
+    tb = build_gpu(w.fgrams, w.lengths, w.ids)
+    ids = torch.empty((cfg.B, cfg.T), dtype=torch.int32, device="cuda")
+    ml = torch.empty((cfg.B, cfg.T), dtype=torch.int8, device="cuda")
+    out = S.embed(tb, dev(w.tokens), max_n, E, fgram_ids=ids, match_len=ml)
+    S.check_ok()
+    np.testing.assert_array_equal(ids.cpu().numpy(), exp_ids)
+    np.testing.assert_array_equal(ml.cpu().numpy(), exp_len)
+    # rows: compare against the generator's rows for the oracle's ids
+    exp_rows = table_rows(cfg, torch.from_numpy(exp_ids.reshape(-1).astype(np.int64)).cuda(),
+                          device="cuda")
+    assert torch.equal(out.view(-1, d).view(torch.int16), exp_rows.view(torch.int16))
+    # and a sample of positions through the oracle's own gather
+    rng = np.random.default_rng(0)
+    pos = rng.integers(0, cfg.n_tok, size=512)
+    sample_ids = exp_ids.reshape(-1)[pos]
+    uniq, inv = np.unique(sample_ids, return_inverse=True)
+    compact = table_rows(cfg, uniq).view(torch.uint8).numpy()
+    exp = oracle.gather(inv.astype(np.int32), compact)
+    got = out.view(cfg.n_tok, -1)[torch.from_numpy(pos).cuda()].cpu().view(torch.uint8).numpy()
+    assert got.tobytes() == exp.tobytes()
