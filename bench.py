@@ -2,10 +2,15 @@
 """Benchmark of the f-gram embedding hot path on one MI355X.
 
 One step is one pass of the whole path over one [B, T] batch already resident
-in HBM: the longest-suffix lookup (scone_lookup) followed by the row gather
-(scone_gather).  The table build is offline and not timed.  Prints one JSON
-line with tokens/s, the gather's achieved bandwidth against the HBM peak, and
-the CPU oracle timed on a bounded sample of the same workload.
+on the device: the longest-suffix lookup (scone_lookup) followed by the row
+gather (scone_gather).  The table build is offline and not timed.  Prints one
+JSON line with tokens/s, the gather's achieved bandwidth against its roofline
+(HBM, or PCIe when the rows live in host-pinned memory), and the CPU oracle
+timed on a bounded sample of the same workload.
+
+Workloads (``--config``): c2_1m (default), c3_10m_k5, tiny (HBM prefill),
+c4_host (rows in host-pinned memory read over PCIe), c5_decode (256
+sequences x 1024 decoding steps of one token each).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config NAME]
 """
@@ -26,8 +31,10 @@ sys.path.insert(0, ROOT)
 
 METRIC = "tokens/sec and gather GB/s (% of HBM peak) for f-gram lookup+gather, 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
+PCIE_PEAK_GBPS = 63.0    # PCIe 5.0 x16, one direction
 DEFAULT_CONFIG = "c2_1m"
 N_BATCHES = 4
+SAMPLE_EVERY = 8
 
 
 def log(*a):
@@ -35,10 +42,13 @@ def log(*a):
 
 
 def describe(cfg) -> str:
+    where = "host-pinned memory" if cfg.placement == "host" else "HBM"
+    shape = (f"{cfg.B} sequences x {cfg.T} decode steps" if cfg.decode
+             else f"queries {cfg.B}x{cfg.T}")
     return (f"{cfg.name}: vocab {cfg.V} Zipf(1.1), {cfg.n_fgrams} f-grams of length "
             f"{cfg.min_len}..{cfg.max_len}, table {cfg.n_rows}x{cfg.d} {cfg.dtype} in "
-            f"{cfg.placement}, queries {cfg.B}x{cfg.T}, {int(cfg.coverage * 100)}% planted "
-            f"coverage, max_n={cfg.max_n}")
+            f"{where}, {shape}, {int(cfg.coverage * 100)}% planted coverage, "
+            f"max_n={cfg.max_n}")
 
 
 def source_sha(name: str) -> str:
@@ -61,8 +71,57 @@ def measured_traffic(config: str, kernel: str, kernel_src: str):
     return rec
 
 
-def cpu_baseline(cfg, w, X0, E, gpu_ids, gpu_outs, min_seconds: float):
-    """Time the oracle (single-threaded) on batch 0, repeated until min_seconds."""
+def build_table(S, torch, w, dev, max_load):
+    fg = torch.from_numpy(w.fgrams).to(dev)
+    ln = torch.from_numpy(w.lengths).to(dev)
+    idv = torch.from_numpy(w.ids).to(dev)
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    table = S.build_fgram_table(fg, ln, idv, max_load=max_load)
+    return table, time.perf_counter() - t
+
+
+def host_rows(S, torch, cfg, dev):
+    """The whole row table in pinned host memory, filled chunk by chunk from
+    the generator on the device."""
+    from workloads import fill_table, torch_dtype
+    t = time.perf_counter()
+    host = S.HostRows(cfg.n_rows, (cfg.d,), torch_dtype(cfg))
+    log(f"pinned {host.nbytes / 1e9:.1f} GB of host memory in {time.perf_counter() - t:.1f} s")
+    ht = host.tensor()
+    chunk = max(1, (1 << 30) // cfg.row_bytes)
+    stage = torch.empty((chunk, cfg.d), dtype=torch_dtype(cfg), device=dev)
+    t = time.perf_counter()
+    for r0 in range(0, cfg.n_rows, chunk):
+        n = min(chunk, cfg.n_rows - r0)
+        fill_table(cfg, stage[:n], row0=r0)
+        ht[r0:r0 + n].copy_(stage[:n])
+        if (r0 // chunk) % 16 == 0:
+            log(f"  filled rows {r0 + n}/{cfg.n_rows}")
+    torch.cuda.synchronize()
+    log(f"filled in {time.perf_counter() - t:.1f} s")
+    del stage
+    return host
+
+
+def h2d_ceiling(torch, dev, nbytes=1 << 30, reps=5):
+    """Measured host-to-device copy rate from pinned memory (GB/s)."""
+    src = torch.empty(nbytes, dtype=torch.uint8, pin_memory=True)
+    dst = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    dst.copy_(src, non_blocking=True)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src, non_blocking=True)
+    e1.record()
+    torch.cuda.synchronize()
+    return nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
+
+
+def cpu_baseline(cfg, w, X0, host_np_full, E, gpu_ids, gpu_outs, min_seconds: float):
+    """Time the oracle (single-threaded) on batch 0, repeated until min_seconds,
+    and check the GPU results of batch 0 against it."""
     import torch
     import oracle
     from workloads import table_rows
@@ -70,17 +129,18 @@ def cpu_baseline(cfg, w, X0, E, gpu_ids, gpu_outs, min_seconds: float):
     o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
     build_s = time.perf_counter() - t0
     exp_ids, exp_len = o.lookup(X0, cfg.max_n)
-    full = cfg.n_rows * cfg.row_bytes <= (4 << 30)
-    if full:
-        # the whole row table in host memory, as the paper's in-memory store
-        host = E.cpu()
-        uniq = None
+    uniq = None
+    if host_np_full is not None:
+        host_np, what = host_np_full, "the full host-pinned table"
+    elif cfg.n_rows * cfg.row_bytes <= (4 << 30):
+        host_np, what = E.cpu().view(torch.uint8).numpy(), "the full host table"
     else:
         # only the rows this batch references (the full table is not copied to
         # the host); the id remap to that compact table is timed with the gather
         uniq = np.unique(exp_ids)
         host = table_rows(cfg, torch.from_numpy(uniq.astype(np.int64)), device="cuda").cpu()
-    host_np = host.view(torch.uint8).numpy()
+        host_np = host.view(torch.uint8).numpy()
+        what = f"a compact host table of the {len(uniq)} referenced rows (id remap timed)"
     passes, elapsed = 0, 0.0
     while elapsed < min_seconds or passes == 0:
         t = time.perf_counter()
@@ -90,9 +150,6 @@ def cpu_baseline(cfg, w, X0, E, gpu_ids, gpu_outs, min_seconds: float):
         out = oracle.gather(ids_p, host_np)
         elapsed += time.perf_counter() - t
         passes += 1
-    what = ("the full host table" if full else
-            f"a compact host table of the {len(uniq)} referenced rows (id remap timed)")
-    parity_ids = bool(np.array_equal(gpu_ids, exp_ids))
     parity_rows = [bool(g.view(torch.uint8).cpu().numpy().reshape(out.shape).tobytes()
                         == out.tobytes()) for g in gpu_outs]
     return ({"value": passes * cfg.n_tok / elapsed, "unit": "tokens/s", "cores": 1,
@@ -101,72 +158,38 @@ def cpu_baseline(cfg, w, X0, E, gpu_ids, gpu_outs, min_seconds: float):
                        f"passes of lookup + memcpy gather from {what}; dictionary build "
                        f"({build_s:.1f} s) not timed",
              "seconds": round(elapsed, 3), "build_seconds": round(build_s, 3)},
-            {"ids_bit_exact": parity_ids, "fused_rows_bit_exact": parity_rows[0],
-             "split_rows_bit_exact": parity_rows[1], "positions": int(cfg.n_tok)}, exp_len)
+            {"ids_bit_exact": bool(np.array_equal(gpu_ids, exp_ids)),
+             "split_rows_bit_exact": parity_rows[0], "fused_rows_bit_exact": parity_rows[1],
+             "positions": int(cfg.n_tok)}, exp_len)
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", default=DEFAULT_CONFIG)
-    ap.add_argument("--max-load", type=float, default=0.5)
-    ap.add_argument("--cpu-seconds", type=float, default=10.0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
-                    help="also run a plain device copy of MIB MiB (counter calibration)")
-    args = ap.parse_args()
-
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              f"(run with --gpus 1)", file=sys.stderr)
-        sys.exit(2)
-
+def run_prefill(args, cfg):
     import torch
     import paper_2502_01637_amd as S
-    from workloads import CONFIGS, make_workload, query_batches, fill_table, torch_dtype, \
-        match_stats
+    from workloads import make_workload, query_batches, fill_table, torch_dtype, match_stats
 
-    cfg = CONFIGS[args.config]
-    if cfg.placement != "hbm" or cfg.decode:
-        print(f"config {cfg.name} is not an HBM prefill workload", file=sys.stderr)
-        sys.exit(2)
     dev = torch.device("cuda", 0)
-    torch.cuda.set_device(dev)
-    log("workload:", describe(cfg))
-
+    host = cfg.placement == "host"
     t = time.perf_counter()
     w = make_workload(cfg)
     batches_np = query_batches(w, N_BATCHES)
     log(f"generated in {time.perf_counter() - t:.1f} s")
-    fg = torch.from_numpy(w.fgrams).to(dev)
-    ln = torch.from_numpy(w.lengths).to(dev)
-    idv = torch.from_numpy(w.ids).to(dev)
-    torch.cuda.synchronize()
-    t = time.perf_counter()
-    table = S.build_fgram_table(fg, ln, idv, max_load=args.max_load)
-    build_s = time.perf_counter() - t
-    del fg, ln, idv
-    E = torch.empty((cfg.n_rows, cfg.d), dtype=torch_dtype(cfg), device=dev)
-    fill_table(cfg, E)
+    table, build_s = build_table(S, torch, w, dev, args.max_load)
+    if host:
+        rows = host_rows(S, torch, cfg, dev)
+        E = None
+    else:
+        E = torch.empty((cfg.n_rows, cfg.d), dtype=torch_dtype(cfg), device=dev)
+        fill_table(cfg, E)
+        rows = E
     X = [torch.from_numpy(b).to(dev) for b in batches_np]
     fid = torch.empty((cfg.B, cfg.T), dtype=torch.int32, device=dev)
-    out = torch.empty((cfg.B, cfg.T, cfg.d), dtype=E.dtype, device=dev)
+    out = torch.empty((cfg.B, cfg.T, cfg.d), dtype=torch_dtype(cfg), device=dev)
     torch.cuda.synchronize()
     log(f"table: {table.n} f-grams, {table.capacity} slots x {table.slot_bytes} B, "
-        f"build {build_s * 1e3:.1f} ms; rows {E.numel() * E.element_size() / 1e9:.2f} GB")
-
-    def split_step(k):
-        S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
-        S.gather(fid, E, out=out)
-
-    def fused_step(k):
-        S.embed(table, X[k % N_BATCHES], cfg.max_n, E, out=out)
+        f"build {build_s * 1e3:.1f} ms")
 
     K = args.steps
-
-    sample_every = 8
 
     def timed(path):
         """W warm-up steps, then K timed steps between two synchronisations.
@@ -174,7 +197,11 @@ def main():
         that they barely perturb the wall clock.  Returns (wall seconds,
         per-kernel mean ms list)."""
         for k in range(args.warmup):
-            (split_step if path == "split" else fused_step)(k)
+            if path == "split":
+                S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
+                S.gather(fid, rows, out=out)
+            else:
+                S.embed(table, X[k % N_BATCHES], cfg.max_n, rows, out=out)
         rc = S.check()
         if rc != 0:
             raise SystemExit(f"device error after warmup ({path}): status {rc}")
@@ -184,7 +211,7 @@ def main():
         t0 = time.perf_counter()
         for k in range(K):
             e = None
-            if k % sample_every == 0:
+            if k % SAMPLE_EVERY == 0:
                 e = [torch.cuda.Event(enable_timing=True) for _ in range(nk + 1)]
                 ev.append(e)
                 e[0].record()
@@ -192,9 +219,9 @@ def main():
                 S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
                 if e:
                     e[1].record()
-                S.gather(fid, E, out=out)
+                S.gather(fid, rows, out=out)
             else:
-                S.embed(table, X[k % N_BATCHES], cfg.max_n, E, out=out)
+                S.embed(table, X[k % N_BATCHES], cfg.max_n, rows, out=out)
             if e:
                 e[nk].record()
         torch.cuda.synchronize()
@@ -221,13 +248,13 @@ def main():
     gen.manual_seed(cfg.seed)
     uid = torch.randint(0, cfg.n_rows, (cfg.B, cfg.T), dtype=torch.int32, device=dev,
                         generator=gen)
-    for _ in range(3):
-        S.gather(uid, E, out=out)
+    for _ in range(2):
+        S.gather(uid, rows, out=out)
     torch.cuda.synchronize()
     ue = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     ue[0].record()
     for _ in range(K):
-        S.gather(uid, E, out=out)
+        S.gather(uid, rows, out=out)
     ue[1].record()
     torch.cuda.synchronize()
     uniform_ms = ue[0].elapsed_time(ue[1]) / K
@@ -243,11 +270,26 @@ def main():
 
     # Batch 0 once more for the parity check and the match statistics.
     fid0, ml0 = S.lookup(table, X[0], cfg.max_n, want_len=True)
-    out0 = S.gather(fid0, E)
-    out0f = S.embed(table, X[0], cfg.max_n, E)
+    out0 = S.gather(fid0, rows)
+    out0f = S.embed(table, X[0], cfg.max_n, rows)
     if S.check() != 0:
         raise SystemExit("device error in parity pass")
     torch.cuda.synchronize()
+
+    if host:
+        # rows cross PCIe once; the output is written to HBM
+        read_bytes = cfg.n_tok * cfg.row_bytes
+        pcie = read_bytes / (gather_ms * 1e-3) / 1e9
+        ceiling = h2d_ceiling(torch, dev)
+        bound, peak, rate = "pcie", PCIE_PEAK_GBPS, pcie
+        extra = {"pcie_read_GBps": pcie, "h2d_copy_ceiling_GBps": ceiling,
+                 "pct_of_h2d_ceiling": 100.0 * pcie / ceiling,
+                 "pcie_inclusive_tokens_per_s": value}
+        alg_bytes = read_bytes
+    else:
+        bound, peak, rate = "hbm", HBM_PEAK_GBPS, achieved
+        extra = {}
+        alg_bytes = gather_bytes
 
     result = {
         "metric": METRIC,
@@ -264,7 +306,7 @@ def main():
         "data": "synthetic (seeded Zipf(1.1) tokens, planted f-grams, counter-based rows)",
         "config": {"workload": describe(cfg), "B": cfg.B, "T": cfg.T, "tokens": cfg.n_tok,
                    "n_fgrams": cfg.n_fgrams, "max_n": cfg.max_n, "d": cfg.d,
-                   "row_bytes": cfg.row_bytes, "placement": "hbm",
+                   "row_bytes": cfg.row_bytes, "placement": cfg.placement,
                    "hash_slots": table.capacity, "slot_bytes": table.slot_bytes,
                    "rotating_batches": N_BATCHES},
         "path": "scone_lookup + scone_gather",
@@ -281,13 +323,13 @@ def main():
                               "pct_hbm_peak": 100.0 * gather_bytes / (uniform_ms * 1e-3) / 1e9
                               / HBM_PEAK_GBPS},
     }
+    result.update(extra)
     traffic = measured_traffic(cfg.name, "gather", "gather.hip")
     result["roofline"] = {
-        "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-        "frac": achieved / HBM_PEAK_GBPS,
+        "bound": bound, "achieved": rate, "peak": peak, "unit": "GB/s", "frac": rate / peak,
         "traffic": None if traffic is None else traffic["traffic_bytes_per_launch"],
         "kernel": "scone_gather (k_gather_rows)",
-        "algorithmic_bytes_per_launch": gather_bytes,
+        "algorithmic_bytes_per_launch": alg_bytes,
     }
     etraffic = measured_traffic(cfg.name, "embed", "embed.hip")
     result["fused_path"]["traffic"] = (None if etraffic is None
@@ -297,13 +339,194 @@ def main():
     result["build_ms"] = build_s * 1e3
 
     if not args.no_cpu_baseline:
-        cb, parity, exp_len = cpu_baseline(cfg, w, batches_np[0], E, fid0.cpu().numpy(),
-                                           [out0f, out0], args.cpu_seconds)
+        host_np = rows.tensor().view(torch.uint8).numpy() if host else None
+        cb, parity, exp_len = cpu_baseline(cfg, w, batches_np[0], host_np, E,
+                                           fid0.cpu().numpy(), [out0, out0f], args.cpu_seconds)
         parity["match_len_bit_exact"] = bool(np.array_equal(ml, exp_len))
         result["cpu_baseline"] = cb
         result["parity"] = parity
     else:
         result["cpu_baseline"] = None
+    if host:
+        rows.close()
+    return result
+
+
+def run_decode(args, cfg):
+    """Decoding: every step appends one token to each of cfg.B sequences and
+    embeds it (scone_decode_step), cfg.T steps in all, eagerly and replayed
+    from a HIP graph."""
+    import torch
+    import paper_2502_01637_amd as S
+    from workloads import make_workload, fill_table, torch_dtype, match_stats
+
+    dev = torch.device("cuda", 0)
+    t = time.perf_counter()
+    w = make_workload(cfg)
+    log(f"generated in {time.perf_counter() - t:.1f} s")
+    table, build_s = build_table(S, torch, w, dev, args.max_load)
+    E = torch.empty((cfg.n_rows, cfg.d), dtype=torch_dtype(cfg), device=dev)
+    fill_table(cfg, E)
+    Sq, steps = cfg.B, cfg.T
+    cap = cfg.max_n - 1
+    Xs = torch.from_numpy(np.ascontiguousarray(w.tokens.T)).to(dev)   # [steps, Sq]
+    ctx = torch.zeros((Sq, cap), dtype=torch.int32, device=dev)
+    clen = torch.zeros(Sq, dtype=torch.int32, device=dev)
+    ids = torch.empty((steps, Sq), dtype=torch.int32, device=dev)
+    lens = torch.empty((steps, Sq), dtype=torch.int8, device=dev)
+    out = torch.empty((Sq, cfg.d), dtype=E.dtype, device=dev)
+    torch.cuda.synchronize()
+
+    def run_all():
+        clen.fill_(0)
+        for s in range(steps):
+            S.decode_step(table, ctx, clen, Xs[s], cfg.max_n, E, out, fgram_ids=ids[s],
+                          match_len=lens[s])
+
+    # warm-up pass, then the timed eager pass (the host launches every step)
+    run_all()
+    if S.check() != 0:
+        raise SystemExit("device error in decode warm-up")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    run_all()
+    torch.cuda.synchronize()
+    eager_wall = time.perf_counter() - t0
+    if S.check() != 0:
+        raise SystemExit("device error in decode")
+    ids_eager = ids.cpu().numpy()
+
+    # the same steps captured once in a HIP graph and replayed
+    g = torch.cuda.CUDAGraph()
+    clen.fill_(0)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        for s in range(steps):
+            S.decode_step(table, ctx, clen, Xs[s], cfg.max_n, E, out, fgram_ids=ids[s],
+                          match_len=lens[s])
+    replays, graph_times, graph_ev_ms = 3, [], []
+    for r in range(replays):
+        clen.fill_(0)
+        ids.fill_(-1)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record()
+        g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        graph_times.append(time.perf_counter() - t0)
+        graph_ev_ms.append(e0.elapsed_time(e1))
+        if S.check() != 0:
+            raise SystemExit("device error in graph replay")
+        if not np.array_equal(ids.cpu().numpy(), ids_eager):
+            raise SystemExit(f"graph replay {r} differs from the eager decode")
+    graph_wall = min(graph_times)
+    # per step on the device: HIP events around the whole replay (per-launch
+    # events would dominate a step this short)
+    step_us = min(graph_ev_ms) * 1e3 / steps
+
+    tokens = Sq * steps
+    per_step_bytes = Sq * (2 * cfg.row_bytes + 4)
+    kernel_GBps = per_step_bytes / (step_us * 1e-6) / 1e9
+    result = {
+        "metric": METRIC,
+        "value": tokens / graph_wall,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": steps,
+        "ms_per_step": graph_wall * 1e3 / steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded Zipf(1.1) tokens, planted f-grams, counter-based rows)",
+        "config": {"workload": describe(cfg), "sequences": Sq, "decode_steps": steps,
+                   "tokens": tokens, "n_fgrams": cfg.n_fgrams, "max_n": cfg.max_n,
+                   "d": cfg.d, "row_bytes": cfg.row_bytes, "placement": "hbm",
+                   "context_capacity": cap, "hash_slots": table.capacity},
+        "path": "scone_decode_step, one launch per step, replayed from a HIP graph",
+        "graph_us_per_step": graph_wall * 1e6 / steps,
+        "eager_us_per_step": eager_wall * 1e6 / steps,
+        "eager_tokens_per_s": tokens / eager_wall,
+        "device_us_per_step": step_us,
+        "roofline": {"bound": "hbm", "achieved": kernel_GBps, "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": kernel_GBps / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel": "scone_decode_step (k_decode)",
+                     "algorithmic_bytes_per_launch": per_step_bytes,
+                     "note": "2.1 MB per step: launch-latency bound, not bandwidth bound"},
+        "match": match_stats(lens.cpu().numpy(), cfg.max_n),
+        "build_ms": build_s * 1e3,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        from workloads import table_rows
+        t0 = time.perf_counter()
+        o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+        build_o = time.perf_counter() - t0
+        # decode step s of a sequence equals the prefill lookup at position s
+        exp_ids, exp_len = o.lookup(w.tokens, cfg.max_n)
+        uniq = np.unique(exp_ids)
+        compact = table_rows(cfg, torch.from_numpy(uniq.astype(np.int64)),
+                             device="cuda").cpu().view(torch.uint8).numpy()
+        passes, elapsed = 0, 0.0
+        while elapsed < args.cpu_seconds or passes == 0:
+            t = time.perf_counter()
+            ids_p, _ = o.lookup(w.tokens, cfg.max_n)
+            oracle.gather(np.searchsorted(uniq, ids_p).astype(np.int32), compact)
+            elapsed += time.perf_counter() - t
+            passes += 1
+        # rows of the last step (left in `out` by the graph replay), byte for byte
+        last = oracle.gather(np.searchsorted(uniq, exp_ids[:, -1]).astype(np.int32), compact)
+        clen.fill_(0)
+        g.replay()
+        torch.cuda.synchronize()
+        result["cpu_baseline"] = {
+            "value": passes * tokens / elapsed, "unit": "tokens/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"all {tokens} tokens of {describe(cfg)} as one prefill lookup "
+                      f"(equal to decoding them), {passes} passes, memcpy gather from a compact "
+                      f"host table of the {len(uniq)} referenced rows (id remap timed); "
+                      f"dictionary build ({build_o:.1f} s) not timed",
+            "seconds": round(elapsed, 3)}
+        result["parity"] = {
+            "ids_bit_exact": bool(np.array_equal(ids_eager.T, exp_ids)),
+            "match_len_bit_exact": bool(np.array_equal(lens.cpu().numpy().T, exp_len)),
+            "last_step_rows_bit_exact": bool(out.cpu().view(torch.uint8).numpy().tobytes()
+                                             == last.tobytes()),
+            "positions": tokens}
+    else:
+        result["cpu_baseline"] = None
+    return result
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default=DEFAULT_CONFIG)
+    ap.add_argument("--max-load", type=float, default=0.5)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="also run a plain device copy of MIB MiB (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              f"(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from workloads import CONFIGS
+    if args.config not in CONFIGS:
+        raise SystemExit(f"unknown config {args.config}; choose from {sorted(CONFIGS)}")
+    cfg = CONFIGS[args.config]
+    torch.cuda.set_device(0)
+    log("workload:", describe(cfg))
+    result = run_decode(args, cfg) if cfg.decode else run_prefill(args, cfg)
     print(json.dumps(result), flush=True)
 
 

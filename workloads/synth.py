@@ -85,7 +85,9 @@ CONFIGS: Dict[str, Config] = {
     "c3_10m_k5": Config("c3_10m_k5", V=32768, n_fgrams=10_000_000, min_len=2,
                         max_len=5, B=32, T=4096, coverage=0.6, max_n=5, d=2048,
                         dtype="bf16", std=0.02, placement="hbm", seed=1002),
-    "c4_host": Config("c4_host", V=32768, n_fgrams=20_000_000, min_len=2,
+    # Off-accelerator rows: 15M f-grams (61.6 GB of rows) is the largest round
+    # size whose table fits within a 64 GiB limit on pinned host memory.
+    "c4_host": Config("c4_host", V=32768, n_fgrams=15_000_000, min_len=2,
                       max_len=3, B=64, T=2048, coverage=0.5, max_n=3, d=2048,
                       dtype="bf16", std=0.02, placement="host", seed=1003),
     "c5_decode": Config("c5_decode", V=32768, n_fgrams=10_000_000, min_len=2,
@@ -320,15 +322,17 @@ def table_rows(cfg: Config, rows, device="cpu", seed: Optional[int] = None):
     return table_values(seed, r * cfg.d + cols, cfg.std, cfg.dtype)
 
 
-def fill_table(cfg: Config, out, seed: Optional[int] = None, chunk_elems: int = 1 << 27):
-    """Fill a preallocated [n_rows, d] tensor (any device) chunk by chunk."""
+def fill_table(cfg: Config, out, seed: Optional[int] = None, chunk_elems: int = 1 << 27,
+               row0: int = 0):
+    """Fill a preallocated [n, d] tensor (any device) with rows row0 .. row0+n-1."""
     import torch
     seed = cfg.seed if seed is None else seed
     flat = out.view(-1)
     total = flat.numel()
     dev = out.device
+    e0 = row0 * cfg.d
     for s in range(0, total, chunk_elems):
-        e = torch.arange(s, min(total, s + chunk_elems), dtype=torch.int64, device=dev)
+        e = torch.arange(e0 + s, e0 + min(total, s + chunk_elems), dtype=torch.int64, device=dev)
         flat[s:s + e.numel()].copy_(table_values(seed, e, cfg.std, cfg.dtype))
     return out
 
