@@ -1,0 +1,134 @@
+"""Parity at the workloads' full sizes, in the launch configuration bench.py times.
+
+Every position's id and match length is compared with the oracle's.  Rows are
+compared at every position against the generator's rows for the oracle's ids
+(the row table is a pure function of the row id), and at sampled positions
+through the oracle's own memcpy gather.
+"""
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2502_01637_amd as S
+from gpu_util import build_gpu, dev, device_rows
+from workloads import CONFIGS, make_workload, query_batches, table_rows, torch_dtype, fill_table
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _free_memory():
+    yield
+    gc.collect()
+    if torch.cuda.is_available():
+        torch.cuda.empty_cache()
+
+
+def rows_match_generator(cfg, out, exp_ids, chunk=1 << 15):
+    """out[k] == generator row exp_ids[k] for every k, compared on the device."""
+    flat_ids = exp_ids.reshape(-1)
+    o = out.view(flat_ids.size, -1)
+    for s in range(0, flat_ids.size, chunk):
+        ids = torch.from_numpy(flat_ids[s:s + chunk].astype(np.int64)).cuda()
+        ref = table_rows(cfg, ids, device="cuda")
+        if not torch.equal(o[s:s + chunk].view(torch.int16), ref.view(torch.int16)):
+            return False
+    return True
+
+
+def sampled_oracle_rows(cfg, out, exp_ids, n=2048, seed=0):
+    """Sampled positions through the oracle's gather over generator rows."""
+    flat_ids = exp_ids.reshape(-1)
+    pos = np.random.default_rng(seed).integers(0, flat_ids.size, size=n)
+    uniq, inv = np.unique(flat_ids[pos], return_inverse=True)
+    compact = table_rows(cfg, uniq).view(torch.uint8).numpy()
+    exp = oracle.gather(inv.astype(np.int32), compact)
+    got = out.view(flat_ids.size, -1)[torch.from_numpy(pos).cuda()].cpu().view(torch.uint8)
+    return got.numpy().tobytes() == exp.tobytes()
+
+
+@pytest.mark.parametrize("name", ["c2_1m", "c3_10m_k5"])
+def test_hbm_prefill_full_size(name):
+    cfg = CONFIGS[name]
+    w = make_workload(cfg)
+    o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+    tb = build_gpu(w.fgrams, w.lengths, w.ids, max_load=0.5)
+    E = device_rows(cfg)
+    for k, X in enumerate(query_batches(w, 2)):
+        exp_ids, exp_len = o.lookup(X, cfg.max_n)
+        ids, ml = S.lookup(tb, dev(X), cfg.max_n, want_len=True)
+        out = S.gather(ids, E)
+        S.check_ok()
+        np.testing.assert_array_equal(ids.cpu().numpy(), exp_ids)
+        np.testing.assert_array_equal(ml.cpu().numpy(), exp_len)
+        assert rows_match_generator(cfg, out, exp_ids), (name, k)
+        assert sampled_oracle_rows(cfg, out, exp_ids, seed=k), (name, k)
+        fused = S.embed(tb, dev(X), cfg.max_n, E)
+        S.check_ok()
+        assert torch.equal(fused.view(torch.int16), out.view(torch.int16)), (name, k)
+        del out, fused
+
+
+def test_host_pinned_full_size():
+    cfg = CONFIGS["c4_host"]
+    w = make_workload(cfg)
+    o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+    exp_ids, exp_len = o.lookup(w.tokens, cfg.max_n)
+    tb = build_gpu(w.fgrams, w.lengths, w.ids, max_load=0.5)
+    host = S.HostRows(cfg.n_rows, (cfg.d,), torch_dtype(cfg))
+    try:
+        ht = host.tensor()
+        chunk = (1 << 30) // cfg.row_bytes
+        stage = torch.empty((chunk, cfg.d), dtype=torch_dtype(cfg), device="cuda")
+        for r0 in range(0, cfg.n_rows, chunk):
+            n = min(chunk, cfg.n_rows - r0)
+            fill_table(cfg, stage[:n], row0=r0)
+            ht[r0:r0 + n].copy_(stage[:n])
+        del stage
+        ids, ml = S.lookup(tb, dev(w.tokens), cfg.max_n, want_len=True)
+        out = S.gather(ids, host)
+        S.check_ok()
+        np.testing.assert_array_equal(ids.cpu().numpy(), exp_ids)
+        np.testing.assert_array_equal(ml.cpu().numpy(), exp_len)
+        # every row, through the oracle's gather over the pinned table itself
+        exp = oracle.gather(exp_ids, ht.view(torch.uint8).numpy())
+        assert out.cpu().view(torch.uint8).numpy().tobytes() == exp.tobytes()
+        fused = S.embed(tb, dev(w.tokens), cfg.max_n, host)
+        S.check_ok()
+        assert torch.equal(fused.view(torch.int16), out.view(torch.int16))
+    finally:
+        host.close()
+
+
+def test_decode_full_size():
+    cfg = CONFIGS["c5_decode"]
+    w = make_workload(cfg)
+    o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+    exp_ids, exp_len = o.lookup(w.tokens, cfg.max_n)   # decoding == prefill per position
+    tb = build_gpu(w.fgrams, w.lengths, w.ids, max_load=0.5)
+    E = device_rows(cfg)
+    Sq, steps = cfg.B, cfg.T
+    Xs = torch.from_numpy(np.ascontiguousarray(w.tokens.T)).cuda()
+    ctx = torch.zeros((Sq, cfg.max_n - 1), dtype=torch.int32, device="cuda")
+    clen = torch.zeros(Sq, dtype=torch.int32, device="cuda")
+    ids = torch.empty((steps, Sq), dtype=torch.int32, device="cuda")
+    lens = torch.empty((steps, Sq), dtype=torch.int8, device="cuda")
+    out = torch.empty((Sq, cfg.d), dtype=E.dtype, device="cuda")
+    check_steps = {0, 1, 2, 511, steps - 1}
+    kept = {}
+    for s in range(steps):
+        S.decode_step(tb, ctx, clen, Xs[s], cfg.max_n, E, out, fgram_ids=ids[s],
+                      match_len=lens[s])
+        if s in check_steps:
+            kept[s] = out.clone()
+    S.check_ok()
+    np.testing.assert_array_equal(ids.cpu().numpy().T, exp_ids)
+    np.testing.assert_array_equal(lens.cpu().numpy().T, exp_len)
+    for s, rows in kept.items():
+        assert rows_match_generator(cfg, rows, exp_ids[:, s]), s
+        assert sampled_oracle_rows(cfg, rows, exp_ids[:, s], n=64, seed=s), s
+    # the context after the last step holds each sequence's last max_n-1 tokens
+    np.testing.assert_array_equal(ctx.cpu().numpy(), w.tokens[:, -(cfg.max_n - 1):])
