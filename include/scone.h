@@ -178,6 +178,42 @@ int scone_decode_step(const scone_table_t* table, int32_t* ctx, int32_t* ctx_len
                       void* out, int32_t* fgram_ids, int8_t* match_len, void* stream);
 
 /*
+ * Row gather with split placement: the token rows stay on the accelerator and
+ * the f-gram rows live off it (Section 3.2 keeps T on the accelerator and
+ * offloads F; Section 4.3 stores F in main memory).  Ids in [0, n_near) read
+ * `near_rows` (device memory); ids in [n_near, n_near + n_far) read row
+ * id - n_near of `far_rows` (host-mapped pinned memory).  Each distinct far id
+ * of the call crosses PCIe once: the call dedupes the far ids in `workspace`,
+ * copies those rows into a device staging area, then writes
+ * out[k, :] = row of fgram_ids[k] from device memory.  The result equals
+ * scone_gather over the concatenated table.
+ *
+ *  fgram_ids   [n_tok] int32; an id outside [0, n_near + n_far) raises
+ *              SCONE_EROW via scone_check and zeroes its output row.
+ *  near_rows   [n_near, row_bytes] device memory; far_rows [n_far, row_bytes]
+ *              host-mapped (scone_host_alloc).  n_near + n_far <= 2^31.
+ *  row_bytes   a multiple of 16; every pointer 16-byte aligned (else
+ *              SCONE_EINVAL).
+ *  out         [n_tok, row_bytes] device output.
+ *  workspace   device scratch of at least scone_gather_split_workspace(n_tok,
+ *              row_bytes) bytes (else SCONE_EINVAL), caller-owned, reusable
+ *              across calls that do not overlap.
+ *  n_unique    device int32 receiving the number of distinct far ids (the
+ *              rows that crossed PCIe), or NULL.
+ *
+ * Asynchronous on `stream`; launches kernels only (no memset or copy nodes),
+ * so the call can be captured in a graph.
+ */
+int scone_gather_split(const int32_t* fgram_ids, int64_t n_tok, const void* near_rows,
+                       int64_t n_near, const void* far_rows, int64_t n_far,
+                       int64_t row_bytes, void* out, void* workspace,
+                       int64_t workspace_bytes, int32_t* n_unique, void* stream);
+
+/* Bytes of workspace scone_gather_split needs for n_tok rows of row_bytes, or
+ * -1 for invalid sizes (worst case: every id distinct and far). */
+int64_t scone_gather_split_workspace(int64_t n_tok, int64_t row_bytes);
+
+/*
  * Allocate `bytes` of pinned host memory that kernels can read over PCIe
  * (the off-accelerator row store of Section 4.3).  *host_ptr receives the
  * host address, *device_ptr the address to pass to scone_gather with

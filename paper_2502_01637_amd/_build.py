@@ -6,7 +6,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libscone.so")
-SOURCES = ["runtime.hip", "table_build.hip", "lookup.hip", "gather.hip", "embed.hip", "decode.hip"]
+SOURCES = ["runtime.hip", "table_build.hip", "lookup.hip", "gather.hip", "embed.hip", "decode.hip",
+           "gather_split.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

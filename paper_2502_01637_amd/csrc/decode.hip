@@ -25,26 +25,32 @@ __global__ __launch_bounds__(kDecodeThreads) void k_decode(
     const int64_t s = blockIdx.x;
     const int lane = threadIdx.x;
     int32_t* my_ctx = ctx + s * ctx_cap;
+    // The length, the new token and the whole context are loaded at once (the
+    // context without waiting for its length); probe windows then come from
+    // the lanes holding the context, so a step has three dependent memory
+    // round trips: inputs, one hash bucket, the row.
     int L = ctx_len[s];
-    L = L < 0 ? 0 : (L > ctx_cap ? ctx_cap : L);
     const int32_t nt = new_tok[s];
+    const int32_t cv_raw = lane < ctx_cap ? my_ctx[lane] : 0;
+    L = L < 0 ? 0 : (L > ctx_cap ? ctx_cap : L);
     // seq[0..L] = context (oldest first) followed by the new token
-    const int32_t cv = lane < L ? my_ctx[lane] : 0;
+    const int32_t cv = lane < L ? cv_raw : 0;
 
     bool hit = false;
     int32_t id = 0;
     const int n = max_n - lane;
+    int32_t win[SCONE_MAX_FGRAM_LEN];
+#pragma unroll
+    for (int i = 0; i < SCONE_MAX_FGRAM_LEN; ++i) {
+        const int k = L + 1 - n + i;  // position of window token i in seq
+        const int32_t c = __shfl(cv, k & 63);
+        win[i] = k < L ? c : nt;
+    }
     if (lane < G && n >= 2 && n <= L + 1) {
-        int32_t win[SCONE_MAX_FGRAM_LEN];
         bool ok = true;
 #pragma unroll
-        for (int i = 0; i < SCONE_MAX_FGRAM_LEN; ++i) {
-            if (i < n) {
-                const int k = L + 1 - n + i;
-                win[i] = k < L ? my_ctx[k] : nt;
-                ok &= (win[i] >= 0) & (win[i] < SCONE_TOKEN_LIMIT);
-            }
-        }
+        for (int i = 0; i < SCONE_MAX_FGRAM_LEN; ++i)
+            if (i < n) ok &= (win[i] >= 0) & (win[i] < SCONE_TOKEN_LIMIT);
         if (ok) hit = probe<SB>(slots, mask, pack_key(win, n), id);
     }
     const unsigned long long m = __ballot(hit);

@@ -47,6 +47,10 @@ def _declare(L):
     L.scone_embed.restype = I
     L.scone_decode_step.argtypes = [P, P, P, I32, P, I64, I32, P, I64, I64, I32, P, P, P, P]
     L.scone_decode_step.restype = I
+    L.scone_gather_split.argtypes = [P, I64, P, I64, P, I64, I64, P, P, I64, P, P]
+    L.scone_gather_split.restype = I
+    L.scone_gather_split_workspace.argtypes = [I64, I64]
+    L.scone_gather_split_workspace.restype = I64
     L.scone_host_alloc.argtypes = [I64, ctypes.POINTER(P), ctypes.POINTER(P)]
     L.scone_host_alloc.restype = I
     L.scone_host_free.argtypes = [P]
@@ -196,6 +200,20 @@ class HostRows:
         self.host_ptr, self.device_ptr = hp.value, dp.value
         self._closed = False
 
+    def rows(self, start: int, stop: int) -> "HostRows":
+        """A view of rows [start, stop) sharing this allocation (not owning it)."""
+        if not 0 <= start <= stop <= self.n_rows:
+            raise ValueError("row range out of bounds")
+        v = HostRows.__new__(HostRows)
+        v.n_rows, v.row_shape, v.dtype, v.row_bytes = stop - start, self.row_shape, self.dtype, \
+            self.row_bytes
+        v.nbytes = v.n_rows * v.row_bytes
+        v.host_ptr = self.host_ptr + start * self.row_bytes
+        v.device_ptr = self.device_ptr + start * self.row_bytes
+        v._closed = True  # a view never frees
+        v._owner = self
+        return v
+
     def tensor(self) -> torch.Tensor:
         """A CPU tensor view of the pinned memory (for filling and checking)."""
         buf = (ctypes.c_uint8 * self.nbytes).from_address(self.host_ptr)
@@ -289,6 +307,44 @@ def decode_step(table: Table, ctx: torch.Tensor, ctx_len: torch.Tensor, new_tok:
                                      S, int(max_n), base, n_rows, row_bytes, placement, _ptr(out),
                                      _ptr(fgram_ids), _ptr(match_len), _stream(stream))
     _check(rc, "scone_decode_step")
+    return out
+
+
+def split_workspace_bytes(n_tok: int, row_bytes: int) -> int:
+    """scone_gather_split_workspace."""
+    n = lib().scone_gather_split_workspace(int(n_tok), int(row_bytes))
+    if n < 0:
+        raise ValueError("invalid sizes")
+    return n
+
+
+def gather_split(fgram_ids: torch.Tensor, near_rows: torch.Tensor, far_rows: "HostRows",
+                 workspace: torch.Tensor, out: Optional[torch.Tensor] = None,
+                 n_unique: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """scone_gather_split: ids < len(near_rows) read near_rows (device), the rest
+    read far_rows (pinned host), each distinct far row crossing PCIe once."""
+    _dev_i32(fgram_ids, "fgram_ids")
+    n_tok = fgram_ids.numel()
+    pn, near_ptr, n_near, rb_n, shape_n, dt_n = _rows_arg(near_rows)
+    pf, far_ptr, n_far, rb_f, shape_f, dt_f = _rows_arg(far_rows)
+    if pn != PLACE_HBM or pf != PLACE_HOST:
+        raise TypeError("near_rows must be a CUDA tensor and far_rows HostRows")
+    if rb_n != rb_f or dt_n != dt_f:
+        raise ValueError("near and far rows differ in width or dtype")
+    if workspace.device.type != "cuda" or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous CUDA tensor")
+    if out is None:
+        out = torch.empty(tuple(fgram_ids.shape) + shape_n, dtype=dt_n, device=fgram_ids.device)
+    if not out.is_contiguous() or out.numel() * out.element_size() != n_tok * rb_n:
+        raise ValueError("out must be contiguous with n_tok * row_bytes bytes")
+    if n_unique is not None and (n_unique.dtype != torch.int32 or n_unique.device.type != "cuda"):
+        raise ValueError("n_unique must be a CUDA int32 tensor")
+    with torch.cuda.device(fgram_ids.device):
+        rc = lib().scone_gather_split(_ptr(fgram_ids), n_tok, near_ptr, n_near, far_ptr, n_far,
+                                      rb_n, _ptr(out), _ptr(workspace),
+                                      workspace.numel() * workspace.element_size(),
+                                      _ptr(n_unique), _stream(stream))
+    _check(rc, "scone_gather_split")
     return out
 
 

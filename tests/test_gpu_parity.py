@@ -390,3 +390,46 @@ def test_embed_many_tiles_per_workgroup(max_len, max_n, d, T):
     exp = oracle.gather(inv.astype(np.int32), compact)
     got = out.view(cfg.n_tok, -1)[torch.from_numpy(pos).cuda()].cpu().view(torch.uint8).numpy()
     assert got.tobytes() == exp.tobytes()
+
+
+# ----------------------------------------------------- split placement ----
+
+@pytest.mark.parametrize("d,n_near,n_far,n_tok", [(64, 40, 500, 3000), (1024, 1000, 3000, 777),
+                                                  (8, 3, 7, 1), (2048, 32768, 20000, 4100)])
+def test_gather_split_matches_concatenated_table(d, n_near, n_far, n_tok):
+    rng = np.random.default_rng(d + n_tok)
+    table = rng.integers(-30000, 30000, size=(n_near + n_far, d), dtype=np.int16)
+    # Zipf-like ids: many repeats among the far rows
+    ids = np.minimum(rng.zipf(1.3, size=n_tok) - 1, n_near + n_far - 1).astype(np.int32)
+    ids[::3] = rng.integers(0, n_near + n_far, size=len(ids[::3]))
+    near = dev(table[:n_near]).view(torch.bfloat16)
+    far = S.HostRows(n_far, (d,), torch.bfloat16)
+    try:
+        far.tensor().view(torch.int16).copy_(torch.from_numpy(table[n_near:]))
+        ws = torch.empty(S.split_workspace_bytes(n_tok, 2 * d), dtype=torch.uint8, device="cuda")
+        nu = torch.zeros(1, dtype=torch.int32, device="cuda")
+        for _ in range(2):  # the workspace is reused across calls
+            out = S.gather_split(dev(ids), near, far, ws, n_unique=nu)
+            S.check_ok()
+            assert out.cpu().view(torch.int16).numpy().tobytes() == \
+                oracle.gather(ids, table).tobytes()
+            assert int(nu.item()) == len(np.unique(ids[ids >= n_near]))
+    finally:
+        far.close()
+
+
+def test_gather_split_errors():
+    near = torch.zeros((4, 8), dtype=torch.float32, device="cuda") + 1
+    far = S.HostRows(3, (8,), torch.float32)
+    try:
+        far.tensor().fill_(2)
+        ids = dev(np.array([0, 5, 7, -1, 6], dtype=np.int32))
+        ws = torch.empty(S.split_workspace_bytes(5, 32), dtype=torch.uint8, device="cuda")
+        out = S.gather_split(ids, near, far, ws)
+        assert S.check() == S.scone.EROW
+        got = out.cpu()
+        assert (got[0] == 1).all() and (got[1] == 2).all() and (got[4] == 2).all()
+        assert (got[2] == 0).all() and (got[3] == 0).all()
+        raises_code(S.scone.EINVAL, S.gather_split, ids, near, far, ws[:100])
+    finally:
+        far.close()
