@@ -550,6 +550,67 @@ def run_decode(args, cfg):
     return result
 
 
+def run_tag(args, cfg):
+    """Pre-scan tagging of a corpus of many query batches: match length per
+    token and the histogram, scone_tag (no ids, no rows)."""
+    import torch
+    import paper_2502_01637_amd as S
+    from workloads import make_workload, query_batches
+
+    dev = torch.device("cuda", 0)
+    w = make_workload(cfg)
+    corpus_np = np.concatenate(query_batches(w, args.tag_batches))
+    table, build_s = build_table(S, torch, w, dev, args.max_load)
+    X = torch.from_numpy(corpus_np).to(dev)
+    n = X.numel()
+    ml = torch.empty(X.shape, dtype=torch.int8, device=dev)
+    hist = torch.zeros(S.scone.MAX_FGRAM_LEN + 1, dtype=torch.int64, device=dev)
+    for _ in range(args.warmup):
+        S.tag(table, X, cfg.max_n, match_len=ml, hist=hist)
+    hist.zero_()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        S.tag(table, X, cfg.max_n, match_len=ml, hist=hist)
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    if S.check() != 0:
+        raise SystemExit("device error in tagging")
+    h = hist.cpu().numpy() // args.steps
+    mean_len = float((h * np.arange(len(h))).sum() / max(h.sum(), 1))
+    result = {"metric": "pre-scan tagging tokens/s (longest f-gram length per token), 1 MI355X",
+              "value": n * args.steps / wall, "unit": "tokens/s", "n_gpus": 1,
+              "steps": args.steps, "warmup": args.warmup,
+              "ms_per_step": wall * 1e3 / args.steps, "higher_is_better": True,
+              "scaling": "weak", "vs_baseline": None, "dtype": "int32",
+              "data": "synthetic corpus (seeded Zipf(1.1) tokens, planted f-grams)",
+              "config": {"workload": describe(cfg), "corpus_tokens": n,
+                         "sequences": int(X.shape[0]), "T": int(X.shape[1])},
+              "device_ms_per_pass": e0.elapsed_time(e1) / args.steps,
+              "histogram": {int(k): int(v) for k, v in enumerate(h) if v},
+              "average_match_length": mean_len, "build_ms": build_s * 1e3}
+    if not args.no_cpu_baseline:
+        import oracle
+        o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+        sample = corpus_np[:cfg.B]
+        t0 = time.perf_counter()
+        passes = 0
+        while time.perf_counter() - t0 < args.cpu_seconds or passes == 0:
+            _, exp_len = o.lookup(sample, cfg.max_n)
+            passes += 1
+        el = time.perf_counter() - t0
+        result["cpu_baseline"] = {"value": passes * sample.size / el, "unit": "tokens/s",
+                                  "cores": 1, "kind": "oracle",
+                                  "sample": f"the first {sample.shape[0]} sequences "
+                                            f"({sample.size} tokens), {passes} passes"}
+        result["parity"] = {"match_len_bit_exact": bool(np.array_equal(
+            ml[:cfg.B].cpu().numpy(), exp_len))}
+    return result
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -559,6 +620,9 @@ def main():
     ap.add_argument("--max-load", type=float, default=0.5)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--tag", action="store_true",
+                    help="pre-scan tagging of a corpus of --tag-batches query batches")
+    ap.add_argument("--tag-batches", type=int, default=64)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
@@ -575,7 +639,12 @@ def main():
     cfg = CONFIGS[args.config]
     torch.cuda.set_device(0)
     log("workload:", describe(cfg))
-    result = run_decode(args, cfg) if cfg.decode else run_prefill(args, cfg)
+    if args.tag:
+        result = run_tag(args, cfg)
+    elif cfg.decode:
+        result = run_decode(args, cfg)
+    else:
+        result = run_prefill(args, cfg)
     print(json.dumps(result), flush=True)
 
 

@@ -114,6 +114,24 @@ int scone_lookup(const scone_table_t* table, const int32_t* token_ids, int64_t B
                  void* stream);
 
 /*
+ * Pre-scan tagging (the paper tags every training token with the length of
+ * its longest matching f-gram before training, implementation details in the
+ * appendix; the mean of these lengths is the "average match length" of
+ * Section 4.1): the match lengths of scone_lookup without the ids, plus
+ * their histogram.
+ *
+ *  token_ids  [B, T] int32, as for scone_lookup.
+ *  match_len  [B, T] int8 output (1 = no f-gram), or NULL.
+ *  hist       [SCONE_MAX_FGRAM_LEN + 1] uint64 device array, or NULL;
+ *             hist[n] is INCREASED by the number of positions whose match
+ *             length is n (the caller zeroes it to start a count).
+ *
+ * At least one of match_len and hist must be given.  Asynchronous.
+ */
+int scone_tag(const scone_table_t* table, const int32_t* token_ids, int64_t B, int64_t T,
+              int32_t max_n, int8_t* match_len, uint64_t* hist, void* stream);
+
+/*
  * Row gather (the embedding fetch; Section 1 notes it is a pure memory read):
  * out[k, :] = rows[fgram_ids[k], :] for k < n_tok, copied as raw bytes, so
  * any element type (fp32, bf16, ...) is reproduced bit for bit.

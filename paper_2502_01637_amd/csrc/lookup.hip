@@ -18,9 +18,12 @@ template <int SB, int G>
 __global__ __launch_bounds__(kTileThreads) void k_lookup(
     const typename SlotOps<SB>::Slot* __restrict__ slots, uint64_t mask,
     const int32_t* __restrict__ X, int64_t T, int max_n, int64_t tiles_per_row,
-    int32_t* __restrict__ ids_out, int8_t* __restrict__ len_out, unsigned* __restrict__ err) {
+    int32_t* __restrict__ ids_out, int8_t* __restrict__ len_out,
+    unsigned long long* __restrict__ hist, unsigned* __restrict__ err) {
     constexpr int P = TileShape<G>::kPositions;
     __shared__ int32_t s_tok[P + kMaxHalo];
+    __shared__ unsigned s_hist[SCONE_MAX_FGRAM_LEN + 1];
+    if (hist && threadIdx.x <= SCONE_MAX_FGRAM_LEN) s_hist[threadIdx.x] = 0;
     const int64_t b = blockIdx.x / tiles_per_row;
     const int64_t t0 = (blockIdx.x - b * tiles_per_row) * (int64_t)P;
     stage_tokens(s_tok, X + b * T, T, t0, P, max_n - 1);
@@ -34,12 +37,19 @@ __global__ __launch_bounds__(kTileThreads) void k_lookup(
         if (!tok_ok) atomicOr(err, err_bit(SCONE_ETOKEN));
         if (ids_out) ids_out[b * T + t] = id;
         if (len_out) len_out[b * T + t] = (int8_t)len;
+        if (hist) atomicAdd(&s_hist[len], 1u);
+    }
+    if (hist) {  // uniform: the whole workgroup takes this branch or none does
+        __syncthreads();
+        if (threadIdx.x <= SCONE_MAX_FGRAM_LEN && s_hist[threadIdx.x])
+            atomicAdd(hist + threadIdx.x, (unsigned long long)s_hist[threadIdx.x]);
     }
 }
 
 template <int SB, int G>
 hipError_t launch(const scone_table* tb, const int32_t* X, int64_t B, int64_t T, int max_n,
-                  int32_t* ids, int8_t* lens, unsigned* err, hipStream_t st) {
+                  int32_t* ids, int8_t* lens, unsigned long long* hist, unsigned* err,
+                  hipStream_t st) {
     using Slot = typename SlotOps<SB>::Slot;
     constexpr int P = TileShape<G>::kPositions;
     const int64_t tiles = (T + P - 1) / P;
@@ -47,28 +57,30 @@ hipError_t launch(const scone_table* tb, const int32_t* X, int64_t B, int64_t T,
     if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL((k_lookup<SB, G>), dim3((unsigned)grid), dim3(kTileThreads), 0, st,
                        static_cast<const Slot*>(tb->slots), (uint64_t)tb->capacity - 1, X, T,
-                       max_n, tiles, ids, lens, err);
+                       max_n, tiles, ids, lens, hist, err);
     return hipGetLastError();
 }
 
 template <int SB>
 hipError_t dispatch_groups(const scone_table* tb, const int32_t* X, int64_t B, int64_t T,
-                           int max_n, int32_t* ids, int8_t* lens, unsigned* err,
-                           hipStream_t st) {
+                           int max_n, int32_t* ids, int8_t* lens, unsigned long long* hist,
+                           unsigned* err, hipStream_t st) {
     switch (lanes_for(max_n)) {
-        case 1: return launch<SB, 1>(tb, X, B, T, max_n, ids, lens, err, st);
-        case 2: return launch<SB, 2>(tb, X, B, T, max_n, ids, lens, err, st);
-        case 4: return launch<SB, 4>(tb, X, B, T, max_n, ids, lens, err, st);
-        default: return launch<SB, 8>(tb, X, B, T, max_n, ids, lens, err, st);
+        case 1: return launch<SB, 1>(tb, X, B, T, max_n, ids, lens, hist, err, st);
+        case 2: return launch<SB, 2>(tb, X, B, T, max_n, ids, lens, hist, err, st);
+        case 4: return launch<SB, 4>(tb, X, B, T, max_n, ids, lens, hist, err, st);
+        default: return launch<SB, 8>(tb, X, B, T, max_n, ids, lens, hist, err, st);
     }
 }
 
 }  // namespace
 
 hipError_t launch_lookup(const scone_table* tb, const int32_t* X, int64_t B, int64_t T,
-                         int max_n, int32_t* ids, int8_t* lens, unsigned* err, hipStream_t st) {
-    return tb->slot_bytes == 16 ? dispatch_groups<16>(tb, X, B, T, max_n, ids, lens, err, st)
-                                : dispatch_groups<32>(tb, X, B, T, max_n, ids, lens, err, st);
+                         int max_n, int32_t* ids, int8_t* lens, unsigned* err, hipStream_t st,
+                         unsigned long long* hist) {
+    return tb->slot_bytes == 16
+               ? dispatch_groups<16>(tb, X, B, T, max_n, ids, lens, hist, err, st)
+               : dispatch_groups<32>(tb, X, B, T, max_n, ids, lens, hist, err, st);
 }
 
 }  // namespace scone
@@ -89,6 +101,28 @@ extern "C" int scone_lookup(const scone_table_t* table, const int32_t* token_ids
     const int eff = max_n < table->max_len ? max_n : table->max_len;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const hipError_t e = launch_lookup(table, token_ids, B, T, eff, fgram_ids, match_len, err, st);
+    if (e == hipErrorInvalidConfiguration) return SCONE_EINVAL;
+    return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
+}
+
+// Pre-scan tagging: the lookup's match lengths and their histogram, without ids.
+extern "C" int scone_tag(const scone_table_t* table, const int32_t* token_ids, int64_t B,
+                         int64_t T, int32_t max_n, int8_t* match_len, uint64_t* hist,
+                         void* stream) {
+    using namespace scone;
+    if (!table || B < 0 || T < 0 || max_n < 1) return SCONE_EINVAL;
+    if (B > 0 && T > ((int64_t)1 << 62) / B) return SCONE_EINVAL;
+    if (B * T == 0) return SCONE_OK;
+    if (!token_ids || (!match_len && !hist)) return SCONE_EINVAL;
+    int dev = 0;
+    SCONE_HIP_TRY(hipGetDevice(&dev));
+    if (dev != table->device) return SCONE_EINVAL;
+    unsigned* err = device_error_word();
+    if (!err) return SCONE_EHIP;
+    const int eff = max_n < table->max_len ? max_n : table->max_len;
+    const hipError_t e = launch_lookup(table, token_ids, B, T, eff, nullptr, match_len, err,
+                                       static_cast<hipStream_t>(stream),
+                                       reinterpret_cast<unsigned long long*>(hist));
     if (e == hipErrorInvalidConfiguration) return SCONE_EINVAL;
     return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
 }

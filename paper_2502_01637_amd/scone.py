@@ -47,6 +47,8 @@ def _declare(L):
     L.scone_embed.restype = I
     L.scone_decode_step.argtypes = [P, P, P, I32, P, I64, I32, P, I64, I64, I32, P, P, P, P]
     L.scone_decode_step.restype = I
+    L.scone_tag.argtypes = [P, P, I64, I64, I32, P, P, P]
+    L.scone_tag.restype = I
     L.scone_gather_split.argtypes = [P, I64, P, I64, P, I64, I64, P, P, I64, P, P]
     L.scone_gather_split.restype = I
     L.scone_gather_split_workspace.argtypes = [I64, I64]
@@ -179,6 +181,28 @@ def lookup(table: Table, token_ids: torch.Tensor, max_n: int,
                                 _ptr(fgram_ids), _ptr(match_len), _stream(stream))
     _check(rc, "scone_lookup")
     return fgram_ids, match_len
+
+
+def tag(table: Table, token_ids: torch.Tensor, max_n: int,
+        match_len: Optional[torch.Tensor] = None, hist: Optional[torch.Tensor] = None,
+        want_len: bool = True, stream=None):
+    """scone_tag: match lengths [B, T] int8 and/or an accumulated histogram
+    (int64 tensor of MAX_FGRAM_LEN + 1 counts, indexed by length)."""
+    _dev_i32(token_ids, "token_ids", 2)
+    B, T = token_ids.shape
+    if match_len is None and want_len:
+        match_len = torch.empty((B, T), dtype=torch.int8, device=token_ids.device)
+    if match_len is not None and (match_len.dtype != torch.int8 or match_len.numel() != B * T
+                                  or not match_len.is_contiguous()):
+        raise ValueError("match_len must be a contiguous int8 tensor of B*T elements")
+    if hist is not None and (hist.dtype != torch.int64 or hist.numel() != MAX_FGRAM_LEN + 1
+                             or hist.device.type != "cuda" or not hist.is_contiguous()):
+        raise ValueError("hist must be a contiguous CUDA int64 tensor of MAX_FGRAM_LEN+1")
+    with torch.cuda.device(token_ids.device):
+        rc = lib().scone_tag(table.handle, _ptr(token_ids), B, T, int(max_n), _ptr(match_len),
+                             _ptr(hist), _stream(stream))
+    _check(rc, "scone_tag")
+    return match_len, hist
 
 
 class HostRows:

@@ -433,3 +433,23 @@ def test_gather_split_errors():
         raises_code(S.scone.EINVAL, S.gather_split, ids, near, far, ws[:100])
     finally:
         far.close()
+
+
+# ------------------------------------------------------- pre-scan tagger --
+
+@pytest.mark.parametrize("name,max_n", [("tiny", 3), ("c3_10m_k5", 5), ("c3_10m_k5", 3)])
+def test_tag_lengths_and_histogram(name, max_n):
+    cfg = scaled(CONFIGS[name], n_fgrams=min(CONFIGS[name].n_fgrams, 40_000), B=7, T=3001)
+    w = make_workload(cfg)
+    o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+    _, exp_len = o.lookup(w.tokens, max_n)
+    tb = build_gpu(w.fgrams, w.lengths, w.ids)
+    hist = torch.zeros(S.scone.MAX_FGRAM_LEN + 1, dtype=torch.int64, device="cuda")
+    ml, _ = S.tag(tb, dev(w.tokens), max_n, hist=hist)
+    S.tag(tb, dev(w.tokens), max_n, hist=hist, want_len=False)  # accumulates
+    S.check_ok()
+    np.testing.assert_array_equal(ml.cpu().numpy(), exp_len)
+    expected = 2 * np.bincount(exp_len.reshape(-1).astype(np.int64),
+                               minlength=S.scone.MAX_FGRAM_LEN + 1)
+    np.testing.assert_array_equal(hist.cpu().numpy(), expected)
+    raises_code(S.scone.EINVAL, S.tag, tb, dev(w.tokens), max_n, want_len=False)
