@@ -232,6 +232,32 @@ int scone_gather_split(const int32_t* fgram_ids, int64_t n_tok, const void* near
 int64_t scone_gather_split_workspace(int64_t n_tok, int64_t row_bytes);
 
 /*
+ * F-gram discovery (Algorithm 3: count every n-gram, n = 2..max_len, of all
+ * sequences and keep the S most frequent; ties at the cut are broken in an
+ * unspecified order, as Algorithm 3 allows).  It follows the efficient form of
+ * Section 3.1: one counting scan per n, and from the second scan on an n-gram
+ * is kept only when it occurs at least min_count times (the paper uses 5);
+ * all 2-grams are kept.  With min_count = 1 the result is Algorithm 3's.
+ * n-grams never cross from one sequence into the next.
+ *
+ *  token_ids  [B, T] int32 (each in [0, SCONE_TOKEN_LIMIT), else
+ *             SCONE_ETOKEN); B * T < 2^31.
+ *  max_len    K, in [2, SCONE_MAX_FGRAM_LEN].
+ *  S          the number of f-grams wanted.
+ *  fgrams     [S, max_len] int32 output, row k holding f-gram k oldest first,
+ *             padded with -1; lengths [S] and counts [S] int32 outputs.
+ *  n_found    host pointer receiving min(S, number of candidates); only that
+ *             many rows are written.
+ *
+ * The output is ready for scone_build_fgram_table (ids are the caller's
+ * choice).  Synchronous; allocates and frees its own device scratch
+ * (about 16 * 2 * B * T bytes of counting table plus per-scan arrays).
+ */
+int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_t T, int32_t max_len,
+                          int32_t min_count, int64_t S, int32_t* fgrams, int32_t* lengths,
+                          int32_t* counts, int64_t* n_found, void* stream);
+
+/*
  * Allocate `bytes` of pinned host memory that kernels can read over PCIe
  * (the off-accelerator row store of Section 4.3).  *host_ptr receives the
  * host address, *device_ptr the address to pass to scone_gather with

@@ -6,8 +6,9 @@ Python binding.
 """
 from . import scone
 from .scone import (SconeError, Table, HostRows, build_fgram_table, lookup, gather, embed,
-                    decode_step, gather_split, split_workspace_bytes, tag, check, check_ok)
+                    decode_step, gather_split, split_workspace_bytes, tag, discover_fgrams,
+                    check, check_ok)
 
 __all__ = ["scone", "SconeError", "Table", "HostRows", "build_fgram_table", "lookup", "gather",
-           "embed", "decode_step", "gather_split", "split_workspace_bytes", "tag", "check",
+           "embed", "decode_step", "gather_split", "split_workspace_bytes", "tag", "discover_fgrams", "check",
            "check_ok"]

@@ -1,0 +1,320 @@
+// F-gram discovery on the device: Algorithm 3 with the K-1 linear scans of
+// Section 3.1.
+//
+// Scan n counts the n-grams of every sequence in an open-addressing table
+// keyed by an exact 64-bit code.  For n = 2 the code is (t0 << 16) | t1.
+// From n = 3 on, an n-gram is counted only when both its (n-1)-prefix and its
+// (n-1)-suffix survived scan n-1 (count >= the minimum count): an n-gram that
+// reaches the minimum appears inside both of them at least as often, so
+// nothing that could survive is skipped.  Every survivor of scan n-1 has a
+// dense id, and an n-gram is coded as (dense id of its prefix << 16) | last
+// token, which is exact and fits 64 bits at any length, so the counting
+// tables need only a 64-bit compare-and-swap.  After each scan the survivors
+// get dense ids and every position learns the id of the survivor ending there
+// (or -1), which is all the next scan reads.
+//
+// The candidates are all 2-grams and the survivors of scans 3..K; the top S by
+// count are found with a threshold search (equal counts at the threshold are
+// taken in an unspecified order, as Algorithm 3 allows) and their tokens are
+// rebuilt by walking the prefix ids back to scan 2.
+#include <vector>
+
+#include "scone_internal.h"
+
+namespace scone {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr uint64_t kEmptyKey = ~0ull;
+
+struct alignas(16) CountSlot {
+    uint64_t key;
+    uint32_t count;
+    int32_t dense;
+};
+
+__device__ __forceinline__ uint64_t count_hash(uint64_t key) {
+    return fmix64(key ^ 0x9E3779B97F4A7C15ULL);
+}
+
+__global__ __launch_bounds__(kThreads) void k_table_clear(CountSlot* __restrict__ t,
+                                                          uint64_t cap) {
+    const uint64_t i = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < cap) {
+        t[i].key = kEmptyKey;
+        t[i].count = 0;
+        t[i].dense = -1;
+    }
+}
+
+// Code of the n-gram ending at flat position i (row position tt), or kEmptyKey
+// when it is not a candidate of scan n.
+__device__ __forceinline__ uint64_t ngram_code(const int32_t* __restrict__ X,
+                                               const int32_t* __restrict__ ids_prev, int64_t i,
+                                               int64_t tt, int n) {
+    if (tt < n - 1) return kEmptyKey;
+    const uint32_t tok = (uint32_t)X[i];
+    if (n == 2) return ((uint64_t)(uint32_t)X[i - 1] << 16) | tok;
+    const int32_t p = ids_prev[i - 1];  // (n-1)-gram ending one earlier: the prefix
+    const int32_t s = ids_prev[i];      // (n-1)-gram ending here: the suffix
+    if (p < 0 || s < 0) return kEmptyKey;
+    return ((uint64_t)p << 16) | tok;
+}
+
+__global__ __launch_bounds__(kThreads) void k_count(const int32_t* __restrict__ X, int64_t BT,
+                                                    int64_t T, int n,
+                                                    const int32_t* __restrict__ ids_prev,
+                                                    CountSlot* __restrict__ t, uint64_t mask,
+                                                    unsigned* __restrict__ status) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= BT) return;
+    if (n == 2) {
+        const int32_t tok = X[i];
+        if (tok < 0 || tok >= SCONE_TOKEN_LIMIT) {
+            atomicOr(status, err_bit(SCONE_ETOKEN));
+            return;
+        }
+    }
+    const int64_t tt = i % T;
+    const uint64_t key = ngram_code(X, ids_prev, i, tt, n);
+    if (key == kEmptyKey) return;
+    if (n == 2 && (X[i - 1] < 0 || X[i - 1] >= SCONE_TOKEN_LIMIT)) return;  // reported there
+    uint64_t s = count_hash(key) & mask;
+    for (uint64_t step = 0; step <= mask; ++step) {
+        const unsigned long long old = atomicCAS(reinterpret_cast<unsigned long long*>(&t[s].key),
+                                                 (unsigned long long)kEmptyKey,
+                                                 (unsigned long long)key);
+        if (old == kEmptyKey || old == key) {
+            atomicAdd(&t[s].count, 1u);
+            return;
+        }
+        s = (s + 1) & mask;
+    }
+    atomicOr(status, err_bit(SCONE_EFULL));
+}
+
+// Dense ids for the survivors (count >= min_count) and, for scan 2, every
+// entry as a candidate; for later scans the survivors are the candidates.
+__global__ __launch_bounds__(kThreads) void k_survivors(
+    CountSlot* __restrict__ t, uint64_t cap, uint32_t min_count, int level, int keep_all,
+    unsigned* __restrict__ n_surv, uint64_t* __restrict__ skey, unsigned* __restrict__ n_cand,
+    uint64_t* __restrict__ cand_key, uint32_t* __restrict__ cand_count,
+    int8_t* __restrict__ cand_level, unsigned* __restrict__ max_count) {
+    const uint64_t s = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (s >= cap) return;
+    const uint64_t key = t[s].key;
+    if (key == kEmptyKey) return;
+    const uint32_t c = t[s].count;
+    const bool survive = c >= min_count;
+    if (survive) {
+        const unsigned id = atomicAdd(n_surv, 1u);
+        t[s].dense = (int32_t)id;
+        if (skey) skey[id] = key;
+    }
+    if (survive || keep_all) {
+        const unsigned k = atomicAdd(n_cand, 1u);
+        cand_key[k] = key;
+        cand_count[k] = c;
+        cand_level[k] = (int8_t)level;
+        atomicMax(max_count, c);
+    }
+}
+
+// Dense id of the survivor of scan n ending at every position, or -1.
+__global__ __launch_bounds__(kThreads) void k_ids(const int32_t* __restrict__ X, int64_t BT,
+                                                  int64_t T, int n,
+                                                  const int32_t* __restrict__ ids_prev,
+                                                  const CountSlot* __restrict__ t, uint64_t mask,
+                                                  int32_t* __restrict__ ids_cur) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= BT) return;
+    const uint64_t key = ngram_code(X, ids_prev, i, i % T, n);
+    int32_t d = -1;
+    if (key != kEmptyKey) {
+        uint64_t s = count_hash(key) & mask;
+        for (uint64_t step = 0; step <= mask; ++step) {
+            const uint64_t k = t[s].key;
+            if (k == key) {
+                d = t[s].dense;
+                break;
+            }
+            if (k == kEmptyKey) break;
+            s = (s + 1) & mask;
+        }
+    }
+    ids_cur[i] = d;
+}
+
+__global__ __launch_bounds__(kThreads) void k_count_at_least(const uint32_t* __restrict__ cnt,
+                                                             int64_t n, uint32_t c,
+                                                             unsigned long long* __restrict__ out) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const bool hit = i < n && cnt[i] >= c;
+    const unsigned long long m = __ballot(hit);
+    if ((threadIdx.x & 63) == 0 && m) atomicAdd(out, (unsigned long long)__popcll(m));
+}
+
+struct LevelKeys {
+    const uint64_t* skey[SCONE_MAX_FGRAM_LEN + 1];  // survivors' codes by scan
+};
+
+// Emit the selected candidates with their tokens.
+__global__ __launch_bounds__(kThreads) void k_select(
+    const uint64_t* __restrict__ cand_key, const uint32_t* __restrict__ cand_count,
+    const int8_t* __restrict__ cand_level, int64_t n_cand, uint32_t thresh, int64_t n_above,
+    int64_t S, LevelKeys lk, int max_len, unsigned* __restrict__ n_gt,
+    unsigned* __restrict__ n_eq, int32_t* __restrict__ fgrams, int32_t* __restrict__ lengths,
+    int32_t* __restrict__ counts) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= n_cand) return;
+    const uint32_t c = cand_count[i];
+    int64_t pos = -1;
+    if (c > thresh) {
+        pos = atomicAdd(n_gt, 1u);
+    } else if (c == thresh) {
+        const int64_t e = atomicAdd(n_eq, 1u);
+        if (n_above + e < S) pos = n_above + e;
+    }
+    if (pos < 0 || pos >= S) return;
+    const int level = cand_level[i];
+    int32_t tok[SCONE_MAX_FGRAM_LEN];
+    uint64_t key = cand_key[i];
+    for (int L = level; L >= 3; --L) {
+        tok[L - 1] = (int32_t)(key & 0xFFFF);
+        key = lk.skey[L - 1][key >> 16];
+    }
+    tok[1] = (int32_t)(key & 0xFFFF);
+    tok[0] = (int32_t)(key >> 16);
+    int32_t* row = fgrams + pos * (int64_t)max_len;
+    for (int j = 0; j < max_len; ++j) row[j] = j < level ? tok[j] : -1;
+    lengths[pos] = level;
+    counts[pos] = (int32_t)c;
+}
+
+}  // namespace
+}  // namespace scone
+
+extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_t T,
+                                     int32_t max_len, int32_t min_count, int64_t S,
+                                     int32_t* fgrams, int32_t* lengths, int32_t* counts,
+                                     int64_t* n_found, void* stream) {
+    using namespace scone;
+    if (!n_found) return SCONE_EINVAL;
+    *n_found = 0;
+    if (B < 0 || T < 0 || S < 0 || min_count < 1) return SCONE_EINVAL;
+    if (max_len < 2 || max_len > SCONE_MAX_FGRAM_LEN) return SCONE_EINVAL;
+    if (B > 0 && T > ((int64_t)1 << 40) / B) return SCONE_EINVAL;
+    const int64_t BT = B * T;
+    if (BT >= ((int64_t)1 << 31)) return SCONE_EINVAL;  // dense ids and counters are 32-bit
+    if (BT == 0 || S == 0) return SCONE_OK;
+    if (!token_ids || !fgrams || !lengths || !counts) return SCONE_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+
+    uint64_t cap = 64;
+    while ((int64_t)cap < 2 * BT) cap <<= 1;
+    const uint64_t mask = cap - 1;
+    const int64_t cand_cap = BT * (int64_t)(max_len - 1);
+
+    // Device scratch, freed before returning (the call is synchronous).
+    std::vector<void*> allocs;
+    auto grab = [&](size_t bytes) -> void* {
+        void* p = nullptr;
+        if (hipMalloc(&p, bytes ? bytes : 16) != hipSuccess) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        allocs.push_back(p);
+        return p;
+    };
+    auto release = [&]() {
+        (void)hipStreamSynchronize(st);
+        for (void* p : allocs) (void)hipFree(p);
+    };
+    CountSlot* table = static_cast<CountSlot*>(grab(cap * sizeof(CountSlot)));
+    int32_t* ids_a = static_cast<int32_t*>(grab(BT * sizeof(int32_t)));
+    int32_t* ids_b = static_cast<int32_t*>(grab(BT * sizeof(int32_t)));
+    uint64_t* cand_key = static_cast<uint64_t*>(grab(cand_cap * sizeof(uint64_t)));
+    uint32_t* cand_count = static_cast<uint32_t*>(grab(cand_cap * sizeof(uint32_t)));
+    int8_t* cand_level = static_cast<int8_t*>(grab(cand_cap));
+    unsigned* ctr = static_cast<unsigned*>(grab(16 * sizeof(unsigned)));
+    unsigned long long* acc = static_cast<unsigned long long*>(grab(sizeof(unsigned long long)));
+    LevelKeys lk{};
+    uint64_t* skeys[SCONE_MAX_FGRAM_LEN + 1] = {};
+    for (int L = 2; L < max_len; ++L) {
+        skeys[L] = static_cast<uint64_t*>(grab(BT * sizeof(uint64_t)));
+        lk.skey[L] = skeys[L];
+    }
+    for (void* p : allocs)
+        if (!p) {
+            release();
+            return SCONE_ENOMEM;
+        }
+    // ctr: [0] status, [1] survivors, [2] candidates, [3] max count, [4] n_gt, [5] n_eq
+    int rc = SCONE_OK;
+    const unsigned g_cap = (unsigned)((cap + kThreads - 1) / kThreads);
+    const unsigned g_bt = (unsigned)((BT + kThreads - 1) / kThreads);
+    if (hipMemsetAsync(ctr, 0, 16 * sizeof(unsigned), st) != hipSuccess) rc = SCONE_EHIP;
+    int32_t* ids_prev = ids_a;
+    int32_t* ids_cur = ids_b;
+    for (int n = 2; n <= max_len && rc == SCONE_OK; ++n) {
+        hipLaunchKernelGGL(k_table_clear, dim3(g_cap), dim3(kThreads), 0, st, table, cap);
+        hipLaunchKernelGGL(k_count, dim3(g_bt), dim3(kThreads), 0, st, token_ids, BT, T, n,
+                           ids_prev, table, mask, ctr + 0);
+        if (hipMemsetAsync(ctr + 1, 0, sizeof(unsigned), st) != hipSuccess) rc = SCONE_EHIP;
+        hipLaunchKernelGGL(k_survivors, dim3(g_cap), dim3(kThreads), 0, st, table, cap,
+                           (uint32_t)min_count, n, n == 2 ? 1 : 0, ctr + 1,
+                           n < max_len ? skeys[n] : nullptr, ctr + 2, cand_key, cand_count,
+                           cand_level, ctr + 3);
+        if (n < max_len) {
+            hipLaunchKernelGGL(k_ids, dim3(g_bt), dim3(kThreads), 0, st, token_ids, BT, T, n,
+                               ids_prev, table, mask, ids_cur);
+            int32_t* tmp = ids_prev;
+            ids_prev = ids_cur;
+            ids_cur = tmp;
+        }
+        if (hipGetLastError() != hipSuccess) rc = SCONE_EHIP;
+    }
+    unsigned h[4] = {0, 0, 0, 0};
+    if (rc == SCONE_OK &&
+        (hipMemcpyAsync(h, ctr, sizeof(h), hipMemcpyDeviceToHost, st) != hipSuccess ||
+         hipStreamSynchronize(st) != hipSuccess))
+        rc = SCONE_EHIP;
+    if (rc == SCONE_OK && h[0]) rc = (h[0] & err_bit(SCONE_ETOKEN)) ? SCONE_ETOKEN : SCONE_EFULL;
+    const int64_t n_cand = h[2];
+    const uint32_t max_c = h[3];
+    // Threshold: the largest count c with at least S candidates counting >= c.
+    auto at_least = [&](uint32_t c, int64_t& out) -> bool {
+        unsigned long long v = 0;
+        if (hipMemsetAsync(acc, 0, sizeof(v), st) != hipSuccess) return false;
+        hipLaunchKernelGGL(k_count_at_least, dim3((unsigned)((n_cand + kThreads - 1) / kThreads)),
+                           dim3(kThreads), 0, st, cand_count, n_cand, c, acc);
+        if (hipMemcpyAsync(&v, acc, sizeof(v), hipMemcpyDeviceToHost, st) != hipSuccess ||
+            hipStreamSynchronize(st) != hipSuccess)
+            return false;
+        out = (int64_t)v;
+        return true;
+    };
+    uint32_t thresh = 0;   // every candidate counts >= 1 > 0
+    int64_t n_above = 0;   // candidates counting > thresh
+    if (rc == SCONE_OK && n_cand > S) {
+        uint32_t lo = 1, hi = max_c;  // at_least(lo) = n_cand >= S
+        while (lo < hi && rc == SCONE_OK) {
+            const uint32_t mid = lo + (hi - lo + 1) / 2;
+            int64_t k = 0;
+            if (!at_least(mid, k)) rc = SCONE_EHIP;
+            else if (k >= S) lo = mid;
+            else hi = mid - 1;
+        }
+        thresh = lo;
+        if (rc == SCONE_OK && thresh < max_c && !at_least(thresh + 1, n_above)) rc = SCONE_EHIP;
+    }
+    if (rc == SCONE_OK && n_cand > 0) {
+        hipLaunchKernelGGL(k_select, dim3((unsigned)((n_cand + kThreads - 1) / kThreads)),
+                           dim3(kThreads), 0, st, cand_key, cand_count, cand_level, n_cand, thresh,
+                           n_above, S, lk, max_len, ctr + 4, ctr + 5, fgrams, lengths, counts);
+        if (hipGetLastError() != hipSuccess) rc = SCONE_EHIP;
+    }
+    release();
+    if (rc == SCONE_OK) *n_found = n_cand < S ? n_cand : S;
+    return rc;
+}

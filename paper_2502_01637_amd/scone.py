@@ -47,6 +47,9 @@ def _declare(L):
     L.scone_embed.restype = I
     L.scone_decode_step.argtypes = [P, P, P, I32, P, I64, I32, P, I64, I64, I32, P, P, P, P]
     L.scone_decode_step.restype = I
+    L.scone_discover_fgrams.argtypes = [P, I64, I64, I32, I32, I64, P, P, P,
+                                        ctypes.POINTER(I64), P]
+    L.scone_discover_fgrams.restype = I
     L.scone_tag.argtypes = [P, P, I64, I64, I32, P, P, P]
     L.scone_tag.restype = I
     L.scone_gather_split.argtypes = [P, I64, P, I64, P, I64, I64, P, P, I64, P, P]
@@ -203,6 +206,27 @@ def tag(table: Table, token_ids: torch.Tensor, max_n: int,
                              _ptr(hist), _stream(stream))
     _check(rc, "scone_tag")
     return match_len, hist
+
+
+def discover_fgrams(token_ids: torch.Tensor, max_len: int, S: int, min_count: int = 5,
+                    stream=None):
+    """scone_discover_fgrams: the S most frequent n-grams (2 <= n <= max_len) of
+    the [B, T] token matrix.  Returns (fgrams [n, max_len], lengths [n],
+    counts [n]) as CUDA int32 tensors, n = min(S, candidates)."""
+    _dev_i32(token_ids, "token_ids", 2)
+    B, T = token_ids.shape
+    dev = token_ids.device
+    fg = torch.empty((max(S, 1), max_len), dtype=torch.int32, device=dev)
+    ln = torch.empty(max(S, 1), dtype=torch.int32, device=dev)
+    ct = torch.empty(max(S, 1), dtype=torch.int32, device=dev)
+    n = ctypes.c_int64()
+    with torch.cuda.device(dev):
+        rc = lib().scone_discover_fgrams(_ptr(token_ids), B, T, int(max_len), int(min_count),
+                                         int(S), _ptr(fg), _ptr(ln), _ptr(ct), ctypes.byref(n),
+                                         _stream(stream))
+    _check(rc, "scone_discover_fgrams")
+    k = n.value
+    return fg[:k], ln[:k], ct[:k]
 
 
 class HostRows:

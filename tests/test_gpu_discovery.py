@@ -1,0 +1,96 @@
+"""GPU f-gram discovery against the discovery oracle.
+
+Equal counts at the cut may be broken either way (Algorithm 3 breaks ties
+arbitrarily), so a result is checked for what is unique: its size, that every
+f-gram is a real candidate with the oracle's count, and that no candidate
+counting more than the smallest kept count was left out.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import discovery
+import paper_2502_01637_amd as S
+from gpu_util import build_gpu, dev
+from workloads import CONFIGS, make_workload, scaled, query_batches
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _clean_error_word():
+    S.check()
+    yield
+    assert S.check() == S.scone.OK
+
+
+def check_top_s(fg, ln, ct, cands, Sn):
+    fg, ln, ct = fg.cpu().numpy(), ln.cpu().numpy(), ct.cpu().numpy()
+    want = min(Sn, len(cands))
+    assert len(ln) == want
+    got = {}
+    for row, L, c in zip(fg, ln, ct):
+        assert 2 <= L <= fg.shape[1] and (row[L:] == -1).all()
+        got[tuple(int(v) for v in row[:L])] = int(c)
+    assert len(got) == want, "duplicate f-grams in the output"
+    oc = dict(cands)
+    for g, c in got.items():
+        assert oc.get(g) == c, (g, c, oc.get(g))
+    if want and want < len(cands):
+        cmin = min(got.values())
+        for g, c in cands:
+            if c > cmin:
+                assert g in got, (g, c, cmin)
+            else:
+                break
+    return got
+
+
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("K,min_count", [(2, 1), (3, 1), (5, 2), (7, 1), (4, 3)])
+def test_discovery_small_random(seed, K, min_count):
+    rng = np.random.default_rng(seed * 31 + K)
+    V = int(rng.integers(2, 7))
+    B, T = int(rng.integers(1, 5)), int(rng.integers(1, 80))
+    X = rng.integers(0, V, size=(B, T)).astype(np.int32)
+    cands = discovery.candidates(X, K, min_count)
+    for Sn in (1, 7, 50, 10 ** 6):
+        fg, ln, ct = S.discover_fgrams(dev(X), K, Sn, min_count)
+        check_top_s(fg, ln, ct, cands, Sn)
+
+
+def test_discovery_zipf_corpus_and_round_trip():
+    cfg = scaled(CONFIGS["c3_10m_k5"], n_fgrams=20_000, B=16, T=2048)
+    w = make_workload(cfg)
+    X = np.concatenate(query_batches(w, 2))
+    cands = discovery.candidates(X, 5, 5)
+    fg, ln, ct = S.discover_fgrams(dev(X), 5, 5000, 5)
+    got = check_top_s(fg, ln, ct, cands, 5000)
+    assert set(len(g) for g in got) >= {2, 3}
+    # the discovered set is a valid f-gram set: it builds and serves lookups
+    ids = np.arange(cfg.V, cfg.V + len(ln), dtype=np.int32)
+    fg_np, ln_np = fg.cpu().numpy(), ln.cpu().numpy()
+    tb = build_gpu(fg_np, ln_np, ids)
+    o = oracle.OracleTable(fg_np, ln_np, ids)
+    exp_ids, exp_len = o.lookup(w.tokens, 5)
+    got_ids, got_len = S.lookup(tb, dev(w.tokens), 5, want_len=True)
+    S.check_ok()
+    np.testing.assert_array_equal(got_ids.cpu().numpy(), exp_ids)
+    np.testing.assert_array_equal(got_len.cpu().numpy(), exp_len)
+
+
+def test_discovery_edges_and_errors():
+    X = np.array([[65535, 65535, 65535, 0, 65535, 65535]], dtype=np.int32)
+    cands = discovery.candidates(X, 4, 1)
+    fg, ln, ct = S.discover_fgrams(dev(X), 4, 100, 1)
+    check_top_s(fg, ln, ct, cands, 100)
+    # sequences shorter than every n-gram: nothing to find
+    fg, ln, ct = S.discover_fgrams(dev(np.zeros((3, 1), np.int32)), 3, 10, 1)
+    assert len(ln) == 0
+    with pytest.raises(S.SconeError) as e:
+        S.discover_fgrams(dev(np.array([[1, 70000, 2]], np.int32)), 3, 10, 1)
+    assert e.value.code == S.scone.ETOKEN
+    with pytest.raises(S.SconeError) as e:
+        S.discover_fgrams(dev(np.array([[1, 2, 2]], np.int32)), 3, 10, 0)
+    assert e.value.code == S.scone.EINVAL
