@@ -119,10 +119,10 @@ def h2d_ceiling(torch, dev, nbytes=1 << 30, reps=5):
     return nbytes * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9
 
 
-def split_placement(S, torch, cfg, table, rows, X, fid, out, K, warmup):
+def split_placement(S, torch, cfg, table, rows, X, fid, outs, K, warmup):
     """Token rows in HBM, f-gram rows in pinned host memory, each distinct
     f-gram row of a batch read over PCIe once (scone_gather_split)."""
-    dev = out.device
+    dev = outs[0].device
     near = rows.tensor()[:cfg.V].to(dev)          # the token rows, copied into HBM
     far = rows.rows(cfg.V, cfg.n_rows)            # the f-gram rows, in place
     ws = torch.empty(S.split_workspace_bytes(cfg.n_tok, cfg.row_bytes), dtype=torch.uint8,
@@ -130,7 +130,7 @@ def split_placement(S, torch, cfg, table, rows, X, fid, out, K, warmup):
     nu = torch.zeros(1, dtype=torch.int32, device=dev)
     for k in range(warmup):
         S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
-        S.gather_split(fid, near, far, ws, out=out, n_unique=nu)
+        S.gather_split(fid, near, far, ws, out=outs[k % N_BATCHES], n_unique=nu)
     if S.check() != 0:
         raise SystemExit("device error in split-placement warm-up")
     ev, uniq = [], []
@@ -144,7 +144,7 @@ def split_placement(S, torch, cfg, table, rows, X, fid, out, K, warmup):
         S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
         if e:
             e[0].record()
-        S.gather_split(fid, near, far, ws, out=out, n_unique=nu)
+        S.gather_split(fid, near, far, ws, out=outs[k % N_BATCHES], n_unique=nu)
         if e:
             e[1].record()
             uniq.append(nu.clone())
@@ -231,7 +231,12 @@ def run_prefill(args, cfg):
         rows = E
     X = [torch.from_numpy(b).to(dev) for b in batches_np]
     fid = torch.empty((cfg.B, cfg.T), dtype=torch.int32, device=dev)
-    out = torch.empty((cfg.B, cfg.T, cfg.d), dtype=torch_dtype(cfg), device=dev)
+    # Step k writes outs[k % N_BATCHES]: together the outputs exceed the 256 MB
+    # last-level cache, so no step overwrites lines the previous one left
+    # dirty there and every step's writes reach HBM.
+    outs = [torch.empty((cfg.B, cfg.T, cfg.d), dtype=torch_dtype(cfg), device=dev)
+            for _ in range(N_BATCHES)]
+    out = outs[0]
     torch.cuda.synchronize()
     log(f"table: {table.n} f-grams, {table.capacity} slots x {table.slot_bytes} B, "
         f"build {build_s * 1e3:.1f} ms")
@@ -246,9 +251,9 @@ def run_prefill(args, cfg):
         for k in range(args.warmup):
             if path == "split":
                 S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
-                S.gather(fid, rows, out=out)
+                S.gather(fid, rows, out=outs[k % N_BATCHES])
             else:
-                S.embed(table, X[k % N_BATCHES], cfg.max_n, rows, out=out)
+                S.embed(table, X[k % N_BATCHES], cfg.max_n, rows, out=outs[k % N_BATCHES])
         rc = S.check()
         if rc != 0:
             raise SystemExit(f"device error after warmup ({path}): status {rc}")
@@ -266,9 +271,9 @@ def run_prefill(args, cfg):
                 S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
                 if e:
                     e[1].record()
-                S.gather(fid, rows, out=out)
+                S.gather(fid, rows, out=outs[k % N_BATCHES])
             else:
-                S.embed(table, X[k % N_BATCHES], cfg.max_n, rows, out=out)
+                S.embed(table, X[k % N_BATCHES], cfg.max_n, rows, out=outs[k % N_BATCHES])
             if e:
                 e[nk].record()
         torch.cuda.synchronize()
@@ -295,13 +300,13 @@ def run_prefill(args, cfg):
     gen.manual_seed(cfg.seed)
     uid = torch.randint(0, cfg.n_rows, (cfg.B, cfg.T), dtype=torch.int32, device=dev,
                         generator=gen)
-    for _ in range(2):
-        S.gather(uid, rows, out=out)
+    for k in range(2):
+        S.gather(uid, rows, out=outs[k % N_BATCHES])
     torch.cuda.synchronize()
     ue = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     ue[0].record()
-    for _ in range(K):
-        S.gather(uid, rows, out=out)
+    for k in range(K):
+        S.gather(uid, rows, out=outs[k % N_BATCHES])
     ue[1].record()
     torch.cuda.synchronize()
     uniform_ms = ue[0].elapsed_time(ue[1]) / K
@@ -324,7 +329,7 @@ def run_prefill(args, cfg):
     torch.cuda.synchronize()
 
     if host:
-        split = split_placement(S, torch, cfg, table, rows, X, fid, out, K, args.warmup)
+        split = split_placement(S, torch, cfg, table, rows, X, fid, outs, K, args.warmup)
     if host:
         # rows cross PCIe once; the output is written to HBM
         read_bytes = cfg.n_tok * cfg.row_bytes
