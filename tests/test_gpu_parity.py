@@ -453,3 +453,51 @@ def test_tag_lengths_and_histogram(name, max_n):
                                minlength=S.scone.MAX_FGRAM_LEN + 1)
     np.testing.assert_array_equal(hist.cpu().numpy(), expected)
     raises_code(S.scone.EINVAL, S.tag, tb, dev(w.tokens), max_n, want_len=False)
+
+
+# ------------------------------------------------------------ HIP graphs --
+
+def test_graph_capture_replays_match_eager():
+    """lookup + gather, the fused kernel and the split gather captured once and
+    replayed several times, with eager work and syncs between replays."""
+    cfg = scaled(CONFIGS["c2_1m"], n_fgrams=20_000, B=4, T=1000, d=256)
+    w = make_workload(cfg)
+    tb = build_gpu(w.fgrams, w.lengths, w.ids)
+    E = device_rows(cfg)
+    X = dev(w.tokens)
+    o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+    exp_ids, _ = o.lookup(w.tokens, cfg.max_n)
+    exp = oracle.gather(exp_ids, E.cpu().view(torch.uint8).numpy())
+    ids = torch.empty((cfg.B, cfg.T), dtype=torch.int32, device="cuda")
+    out_a = torch.empty((cfg.B, cfg.T, cfg.d), dtype=E.dtype, device="cuda")
+    out_b = torch.empty_like(out_a)
+    out_c = torch.empty_like(out_a)
+    near = E[:cfg.V].contiguous()
+    far = S.HostRows(cfg.n_fgrams, (cfg.d,), E.dtype)
+    try:
+        far.tensor().copy_(E[cfg.V:].cpu())
+        ws = torch.empty(S.split_workspace_bytes(cfg.n_tok, cfg.row_bytes), dtype=torch.uint8,
+                         device="cuda")
+        # eager once (also initialises the library's error word outside capture)
+        S.lookup(tb, X, cfg.max_n, fgram_ids=ids)
+        S.gather(ids, E, out=out_a)
+        S.check_ok()
+        g = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            S.lookup(tb, X, cfg.max_n, fgram_ids=ids)
+            S.gather(ids, E, out=out_a)
+            S.embed(tb, X, cfg.max_n, E, out=out_b)
+            S.gather_split(ids, near, far, ws, out=out_c)
+        for r in range(4):
+            for t in (ids, out_a, out_b, out_c):
+                t.view(torch.uint8).fill_(0xA5)      # eager work between replays
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            S.check_ok()
+            np.testing.assert_array_equal(ids.cpu().numpy(), exp_ids)
+            for t in (out_a, out_b, out_c):
+                assert as_bytes(t).tobytes() == exp.tobytes(), r
+    finally:
+        far.close()
