@@ -35,6 +35,7 @@ PCIE_PEAK_GBPS = 63.0    # PCIe 5.0 x16, one direction
 DEFAULT_CONFIG = "c2_1m"
 N_BATCHES = 4
 SAMPLE_EVERY = 8
+COLD_REPS = 10
 
 
 def log(*a):
@@ -311,6 +312,32 @@ def run_prefill(args, cfg):
     torch.cuda.synchronize()
     uniform_ms = ue[0].elapsed_time(ue[1]) / K
 
+    # Cold caches: reading a 1 GiB buffer between repetitions evicts the L2s
+    # and the 256 MB last-level cache, so table, hash slots and tokens all come
+    # from HBM.  The buffer is read, not written, so the caches hold clean
+    # lines and the timed kernels pay no write-back of the flush itself.
+    cold = None
+    if not host:
+        flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        ce = []
+        for k in range(COLD_REPS):
+            flush.amax()
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            e[0].record()
+            S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
+            e[1].record()
+            S.gather(fid, rows, out=outs[k % N_BATCHES])
+            e[2].record()
+            ce.append(e)
+        torch.cuda.synchronize()
+        del flush
+        c_look = float(np.mean([e[0].elapsed_time(e[1]) for e in ce]))
+        c_gath = float(np.mean([e[1].elapsed_time(e[2]) for e in ce]))
+        cold = {"reps": COLD_REPS, "flush_bytes": 1 << 30, "lookup_us": c_look * 1e3,
+                "gather_us": c_gath * 1e3,
+                "gather_GBps": gather_bytes / (c_gath * 1e-3) / 1e9,
+                "device_tokens_per_s": cfg.n_tok / ((c_look + c_gath) * 1e-3)}
+
     if args.copy_calibration:
         n = args.copy_calibration << 20
         src = torch.empty(n, dtype=torch.uint8, device=dev)
@@ -372,6 +399,8 @@ def run_prefill(args, cfg):
                        "ms_per_step": fused_wall * 1e3 / K,
                        "embed_us": embed_ms * 1e3, "embed_GBps": embed_achieved,
                        "embed_pct_hbm_peak": 100.0 * embed_achieved / HBM_PEAK_GBPS},
+        "warm_device_tokens_per_s": cfg.n_tok / ((lookup_ms + gather_ms) * 1e-3),
+        "cold_caches": cold,
         "uniform_id_gather": {"us": uniform_ms * 1e3,
                               "GBps": gather_bytes / (uniform_ms * 1e-3) / 1e9,
                               "pct_hbm_peak": 100.0 * gather_bytes / (uniform_ms * 1e-3) / 1e9
