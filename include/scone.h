@@ -23,8 +23,10 @@
  *    without a sync: asynchronous calls raise them in the device's error
  *    word and report them through scone_check().  After such an error the
  *    contents of the outputs are unspecified.
- *  - No call allocates device memory except scone_build_fgram_table and
- *    scone_host_alloc (and a 4-byte error word per device on first use).
+ *  - No call allocates device memory except scone_build_fgram_table,
+ *    scone_host_alloc and the synchronous offline calls
+ *    scone_discover_fgrams and scone_fgram_model_forward (and a 4-byte error
+ *    word per device on first use).
  *  - All buffers are owned by the caller except the table handle, which the
  *    library owns until scone_table_destroy.
  */
@@ -256,6 +258,69 @@ int64_t scone_gather_split_workspace(int64_t n_tok, int64_t row_bytes);
 int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_t T, int32_t max_len,
                           int32_t min_count, int64_t S, int32_t* fgrams, int32_t* lengths,
                           int32_t* counts, int64_t* n_found, void* stream);
+
+/*
+ * Precompute the f-gram embedding layer (Section 3.2: F caches the f-gram
+ * model's outputs, one row per f-gram; the model maps the token embeddings of
+ * an f-gram to the output at its final token, Algorithm 1's training branch).
+ *
+ * The f-gram model A_fgram is a pre-LayerNorm causal decoder (the paper gives
+ * its sizes through the main-model tables of the appendix, absolute position
+ * embeddings with one row per position up to the longest f-gram, and bf16
+ * parameters; the rest is this library's reading):
+ *     h_i = T(w_i) + pos[i]                          i = 0 (oldest) .. n-1
+ *     per layer:  h += Attn(LN1(h));  h += W2 GELU(W1 LN2(h) + b1) + b2
+ *     F(w) = LNf(h_{n-1})
+ * with causal multi-head attention (scores scaled by 1/sqrt(d / n_heads)),
+ * exact erf GELU, LayerNorm epsilon 1e-5 over the population variance, and
+ * y = x W^T + b for every linear map (W stored [out, in]).  F-grams of equal
+ * length are processed together, unpadded (the paper right-pads a batch to
+ * its longest f-gram; under causal attention the final token never sees a
+ * pad, so the result is the same).
+ *
+ *  fgrams    [n, max_len] int32, row k = f-gram k oldest first (entries past
+ *            lengths[k] are ignored); tokens in [0, vocab) else SCONE_ETOKEN.
+ *  lengths   [n] int32 in [2, max_len] (else SCONE_ELEN, nothing computed).
+ *  row_ids   [n] int32: F(f-gram k) is written to row row_ids[k] of `rows`;
+ *            outside [0, n_rows) -> SCONE_EROW and that row is skipped.
+ *  max_len   K in [2, SCONE_MAX_FGRAM_LEN] = the number of position rows.
+ *  tok_rows  [vocab, d] bf16, the token embedding layer T.  It may be the
+ *            first vocab rows of `rows` (the unified table) as long as no
+ *            row id falls below vocab.
+ *  params    bf16 parameters packed as scone_fgram_model_layout describes:
+ *              pos [max_len, d];
+ *              per layer: ln1_g [d], ln1_b [d], w_qkv [3d, d] (q, k, v
+ *                rows in that order, heads contiguous), b_qkv [3d],
+ *                w_o [d, d], b_o [d], ln2_g [d], ln2_b [d],
+ *                w_fc1 [d_ff, d], b_fc1 [d_ff], w_fc2 [d, d_ff], b_fc2 [d];
+ *              lnf_g [d], lnf_b [d];
+ *            each tensor row-major, starting at a multiple of 128 elements.
+ *  d         d_model, a multiple of 512 up to 4096; d / n_heads must be 64 or
+ *            128; d_ff a multiple of 128; n_layers >= 0 (0 gives
+ *            LNf(T(w_{n-1}) + pos[n-1])).
+ *  rows      [n_rows, d] bf16 output table (device memory).
+ *
+ * tok_rows, params and rows must be 16-byte aligned (else SCONE_EINVAL).
+ * Synchronous: returns after the rows are written, with the first data error
+ * (SCONE_ELEN, SCONE_ETOKEN, SCONE_EROW) or SCONE_OK.  Allocates and frees its
+ * own device scratch: about 65536 * (14 d + 2 d_ff) bytes of activations for
+ * one chunk of same-length f-grams, plus 4 n bytes.
+ */
+int scone_fgram_model_forward(const int32_t* fgrams, const int32_t* lengths,
+                              const int32_t* row_ids, int64_t n, int32_t max_len,
+                              const void* tok_rows, int64_t vocab, const void* params, int32_t d,
+                              int32_t n_heads, int32_t d_ff, int32_t n_layers, void* rows,
+                              int64_t n_rows, void* stream);
+
+/*
+ * Packing of scone_fgram_model_forward's parameters: offsets[k] (elements)
+ * of the k-th tensor in the order listed there (2 + 12 * n_layers + 1
+ * tensors; offsets may be NULL), the tensor count and the total element count
+ * of the blob.  SCONE_EINVAL for unsupported sizes.
+ */
+int scone_fgram_model_layout(int32_t d, int32_t n_heads, int32_t d_ff, int32_t n_layers,
+                             int32_t max_len, int64_t* offsets, int64_t* n_params,
+                             int64_t* total_elems);
 
 /*
  * Allocate `bytes` of pinned host memory that kernels can read over PCIe

@@ -56,6 +56,12 @@ def _declare(L):
     L.scone_gather_split.restype = I
     L.scone_gather_split_workspace.argtypes = [I64, I64]
     L.scone_gather_split_workspace.restype = I64
+    L.scone_fgram_model_forward.argtypes = [P, P, P, I64, I32, P, I64, P, I32, I32, I32, I32,
+                                            P, I64, P]
+    L.scone_fgram_model_forward.restype = I
+    L.scone_fgram_model_layout.argtypes = [I32, I32, I32, I32, I32, ctypes.POINTER(I64),
+                                           ctypes.POINTER(I64), ctypes.POINTER(I64)]
+    L.scone_fgram_model_layout.restype = I
     L.scone_host_alloc.argtypes = [I64, ctypes.POINTER(P), ctypes.POINTER(P)]
     L.scone_host_alloc.restype = I
     L.scone_host_free.argtypes = [P]
@@ -227,6 +233,79 @@ def discover_fgrams(token_ids: torch.Tensor, max_len: int, S: int, min_count: in
     _check(rc, "scone_discover_fgrams")
     k = n.value
     return fg[:k], ln[:k], ct[:k]
+
+
+_LAYER_PARAMS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o", "ln2_g", "ln2_b",
+                 "w_fc1", "b_fc1", "w_fc2", "b_fc2")
+
+
+class FgramModel:
+    """Parameters of an f-gram model packed into one bf16 device blob in the
+    order scone_fgram_model_forward reads them.
+
+    ``params`` maps names to tensors (or arrays) of bf16 values or raw bf16
+    bits (int16/uint16): "pos", "l{i}.<name>" for every layer i and name in
+    ln1_g ln1_b w_qkv b_qkv w_o b_o ln2_g ln2_b w_fc1 b_fc1 w_fc2 b_fc2, then
+    "lnf_g", "lnf_b".  Linear weights are [out_features, in_features]."""
+
+    def __init__(self, params, d: int, n_heads: int, d_ff: int, n_layers: int, max_len: int,
+                 device=None):
+        self.d, self.n_heads, self.d_ff = int(d), int(n_heads), int(d_ff)
+        self.n_layers, self.max_len = int(n_layers), int(max_len)
+        n_par, total = ctypes.c_int64(), ctypes.c_int64()
+        rc = lib().scone_fgram_model_layout(self.d, self.n_heads, self.d_ff, self.n_layers,
+                                            self.max_len, None, ctypes.byref(n_par),
+                                            ctypes.byref(total))
+        _check(rc, "scone_fgram_model_layout")
+        offs = (ctypes.c_int64 * n_par.value)()
+        lib().scone_fgram_model_layout(self.d, self.n_heads, self.d_ff, self.n_layers,
+                                       self.max_len, offs, ctypes.byref(n_par),
+                                       ctypes.byref(total))
+        names = ["pos"] + [f"l{i}.{p}" for i in range(self.n_layers) for p in _LAYER_PARAMS] \
+            + ["lnf_g", "lnf_b"]
+        assert len(names) == n_par.value
+        device = torch.device("cuda", torch.cuda.current_device()) if device is None \
+            else torch.device(device)
+        blob = torch.zeros(total.value, dtype=torch.int16, device=device)
+        for k, name in enumerate(names):
+            v = params[name]
+            t = v if isinstance(v, torch.Tensor) else torch.from_numpy(v)
+            if t.dtype == torch.bfloat16:
+                t = t.view(torch.int16)
+            elif t.dtype == torch.uint16:
+                t = t.view(torch.int16)
+            elif t.dtype != torch.int16:
+                raise TypeError(f"{name}: expected bf16 values or bits, got {t.dtype}")
+            flat = t.reshape(-1)
+            blob[offs[k]:offs[k] + flat.numel()].copy_(flat)
+        self.blob = blob
+        self.device = device
+
+
+def precompute_fgram_rows(model: FgramModel, fgrams: torch.Tensor, lengths: torch.Tensor,
+                          row_ids: torch.Tensor, tok_rows: torch.Tensor, rows: torch.Tensor,
+                          stream=None):
+    """scone_fgram_model_forward: rows[row_ids[k]] = F(f-gram k) (bf16), the
+    f-gram model's output at the last token.  tok_rows [vocab, d] bf16 is the
+    token embedding layer; rows [n_rows, d] bf16 is written in place.
+    Synchronous."""
+    _dev_i32(fgrams, "fgrams", 2)
+    _dev_i32(lengths, "lengths", 1)
+    _dev_i32(row_ids, "row_ids", 1)
+    for name, t in (("tok_rows", tok_rows), ("rows", rows)):
+        if t.device.type != "cuda" or t.dtype != torch.bfloat16 or t.dim() != 2 \
+                or not t.is_contiguous() or t.shape[1] != model.d:
+            raise ValueError(f"{name} must be a contiguous [*, {model.d}] bf16 CUDA tensor")
+    n, K = fgrams.shape
+    if K != model.max_len or lengths.numel() != n or row_ids.numel() != n:
+        raise ValueError("fgrams must be [n, max_len] with n lengths and n row ids")
+    with torch.cuda.device(rows.device):
+        rc = lib().scone_fgram_model_forward(
+            _ptr(fgrams), _ptr(lengths), _ptr(row_ids), n, model.max_len, _ptr(tok_rows),
+            tok_rows.shape[0], model.blob.data_ptr(), model.d, model.n_heads, model.d_ff,
+            model.n_layers, _ptr(rows), rows.shape[0], _stream(stream))
+    _check(rc, "scone_fgram_model_forward")
+    return rows
 
 
 class HostRows:

@@ -70,3 +70,36 @@ def test_binding_rejects_non_device_tensors():
     with pytest.raises(TypeError):
         S.build_fgram_table(torch.zeros((1, 2), dtype=torch.int32),
                             torch.zeros(1, dtype=torch.int32), torch.zeros(1, dtype=torch.int32))
+
+
+def test_fgram_model_layout_and_argument_errors():
+    L = S.scone.lib()
+    E = S.scone.EINVAL
+    n_par, total = ctypes.c_int64(), ctypes.c_int64()
+    for d, h, f, nl, K in [(512, 8, 1024, 2, 7), (1024, 16, 4096, 6, 3), (2048, 16, 8192, 0, 5)]:
+        assert L.scone_fgram_model_layout(d, h, f, nl, K, None, ctypes.byref(n_par),
+                                          ctypes.byref(total)) == S.scone.OK
+        assert n_par.value == 3 + 12 * nl
+        offs = (ctypes.c_int64 * n_par.value)()
+        assert L.scone_fgram_model_layout(d, h, f, nl, K, offs, None, None) == S.scone.OK
+        sizes = [K * d] + [s for _ in range(nl) for s in
+                           (d, d, 3 * d * d, 3 * d, d * d, d, d, d, f * d, f, d * f, d)] + [d, d]
+        o = list(offs)
+        assert o[0] == 0 and all(x % 128 == 0 for x in o)
+        for k in range(len(o) - 1):   # each tensor fits before the next one starts
+            assert o[k] + sizes[k] <= o[k + 1] < o[k] + sizes[k] + 128
+        assert o[-1] + sizes[-1] <= total.value < o[-1] + sizes[-1] + 128
+    # unsupported sizes: d not a multiple of 512, head width not 64/128, d_ff, K
+    for d, h, f, nl, K in [(768, 12, 3072, 1, 3), (512, 16, 1024, 1, 3), (512, 8, 1000, 1, 3),
+                           (512, 8, 1024, 1, 8), (512, 8, 1024, 1, 1), (512, 8, 1024, -1, 3),
+                           (8192, 64, 1024, 1, 3)]:
+        assert L.scone_fgram_model_layout(d, h, f, nl, K, None, None, None) == E
+        assert L.scone_fgram_model_forward(None, None, None, 1, K, None, 10, None, d, h, f, nl,
+                                           None, 10, None) == E
+    # good sizes, bad pointers or counts: rejected before any device work
+    assert L.scone_fgram_model_forward(None, None, None, 1, 3, None, 10, None, 512, 8, 1024, 1,
+                                       None, 10, None) == E
+    assert L.scone_fgram_model_forward(None, None, None, -1, 3, None, 10, None, 512, 8, 1024, 1,
+                                       None, 10, None) == E
+    assert L.scone_fgram_model_forward(None, None, None, 0, 3, None, 10, None, 512, 8, 1024, 1,
+                                       None, 10, None) == S.scone.OK
