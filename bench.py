@@ -32,6 +32,7 @@ sys.path.insert(0, ROOT)
 METRIC = "tokens/sec and gather GB/s (% of HBM peak) for f-gram lookup+gather, 1 MI355X"
 HBM_PEAK_GBPS = 8000.0
 PCIE_PEAK_GBPS = 63.0    # PCIe 5.0 x16, one direction
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak
 DEFAULT_CONFIG = "c2_1m"
 N_BATCHES = 4
 SAMPLE_EVERY = 8
@@ -698,6 +699,98 @@ def run_discover(args, cfg):
     return result
 
 
+def fgram_model_flops(lengths: np.ndarray, d: int, d_ff: int, n_layers: int) -> float:
+    """Algorithmic flops of the f-gram model over f-grams of these lengths: per
+    token and layer 2 (3d^2 + d^2 + 2 d d_ff) for the four products, and
+    4 (i + 1) d for the scores and the weighted sum of position i."""
+    n = lengths.astype(np.float64)
+    tokens = n.sum()
+    attn_per_layer = (4.0 * d * n * (n + 1) / 2).sum()
+    return n_layers * (tokens * 2.0 * (4.0 * d * d + 2.0 * d * d_ff) + attn_per_layer)
+
+
+def run_precompute(args, cfg):
+    """Precompute of the f-gram rows (scone_fgram_model_forward) for the whole
+    f-gram set of a workload, through a 6-layer d_model 1024 f-gram model."""
+    import torch
+    import paper_2502_01637_amd as S
+    from workloads import make_workload, fill_table, torch_dtype
+    from workloads.fgram_model import GPT2_128M, make_params, bf16_bits_to_f64
+
+    if cfg.dtype != "bf16" or cfg.d != GPT2_128M.d or cfg.max_len > GPT2_128M.max_len:
+        raise SystemExit("--precompute needs a bf16 workload with d = 1024 and f-grams up to 3")
+    mc = GPT2_128M
+    dev = torch.device("cuda", 0)
+    w = make_workload(cfg)
+    fg_np = np.ascontiguousarray(w.fgrams[:, :mc.max_len])
+    P = make_params(mc, seed=cfg.seed + 7, recipe="gpt2")
+    model = S.FgramModel(P, mc.d, mc.n_heads, mc.d_ff, mc.n_layers, mc.max_len, device=dev)
+    E = torch.empty((cfg.n_rows, cfg.d), dtype=torch_dtype(cfg), device=dev)
+    fill_table(cfg, E)
+    fg, ln, ids = (torch.from_numpy(a).to(dev) for a in (fg_np, w.lengths, w.ids))
+    tok = E[:cfg.V]
+    for _ in range(args.warmup):
+        S.precompute_fgram_rows(model, fg, ln, ids, tok, E)
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    evs = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        e[0].record(st)
+        S.precompute_fgram_rows(model, fg, ln, ids, tok, E)
+        e[1].record(st)
+        evs.append(e)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dev_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    flops = fgram_model_flops(w.lengths, mc.d, mc.d_ff, mc.n_layers)
+    tflops = flops / (dev_ms * 1e-3) / 1e12
+    n = len(w.lengths)
+    result = {"metric": "f-gram rows precomputed/s (F = A_fgram over every f-gram), 1 MI355X",
+              "value": n * args.steps / wall, "unit": "f-grams/s", "n_gpus": 1,
+              "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps,
+              "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+              "data": "synthetic f-gram set (seeded Zipf(1.1)), random GPT-2-style weights",
+              "config": {"workload": f"{describe(cfg)}; f-gram model d_model {mc.d}, "
+                                     f"{mc.n_heads} heads, ffw {mc.d_ff}, {mc.n_layers} layers",
+                         "n_fgrams": n, "tokens": int(w.lengths.sum()), "d": mc.d,
+                         "d_ff": mc.d_ff, "n_layers": mc.n_layers, "n_heads": mc.n_heads},
+              "device_ms_per_step": dev_ms, "flops_per_step": flops, "TFLOPs": tflops,
+              "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS,
+                           "unit": "TFLOP/s", "frac": tflops / MFMA_BF16_PEAK_TFLOPS,
+                           "traffic": None,
+                           "kernel": "scone_fgram_model_forward (all kernels of one call)",
+                           "algorithmic_flops_per_launch": flops}}
+    # parity on a sample of rows, bar of the GPU parity tests (3 eps(L) per row)
+    from oracle import fgram_model as orc
+    rng = np.random.default_rng(0)
+    sample = rng.choice(n, 32, replace=False)
+    T64 = E[:cfg.V].float().cpu().numpy().astype(np.float64)
+    P64 = {k: bf16_bits_to_f64(v) for k, v in P.items()}
+    ref = orc.forward(fg_np[sample], w.lengths[sample], T64, P64, mc.n_layers, mc.n_heads)
+    got = E[torch.from_numpy(w.ids[sample].astype(np.int64)).to(dev)].float().cpu().numpy()
+    rel = np.linalg.norm(got - ref, axis=1) / np.linalg.norm(ref, axis=1)
+    bar = 3 * 2.0 ** -9 * np.sqrt((5 * mc.n_layers + 2) / 3)
+    result["parity"] = {"sample_rows": len(sample), "max_row_rel_err": float(rel.max()),
+                        "bar": bar, "ok": bool(rel.max() <= bar)}
+    if not args.no_cpu_baseline:
+        cs = rng.choice(n, 64, replace=False)
+        t0 = time.perf_counter()
+        reps = 0
+        while True:
+            orc.forward(fg_np[cs], w.lengths[cs], T64, P64, mc.n_layers, mc.n_heads)
+            reps += 1
+            if time.perf_counter() - t0 >= min(args.cpu_seconds, 10.0):
+                break
+        el = time.perf_counter() - t0
+        result["cpu_baseline"] = {"value": reps * len(cs) / el, "unit": "f-grams/s",
+                                  "cores": torch.get_num_threads(), "kind": "oracle",
+                                  "sample": f"{len(cs)} f-grams, repeated {reps} times, "
+                                            "float64 numpy (BLAS threads)"}
+    return result
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -713,6 +806,8 @@ def main():
     ap.add_argument("--discover", action="store_true",
                     help="f-gram discovery over a corpus of --tag-batches query batches")
     ap.add_argument("--discover-s", type=int, default=1_000_000)
+    ap.add_argument("--precompute", action="store_true",
+                    help="time the precompute of the f-gram rows by the f-gram model")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of MIB MiB (counter calibration)")
     args = ap.parse_args()
@@ -729,7 +824,13 @@ def main():
     cfg = CONFIGS[args.config]
     torch.cuda.set_device(0)
     log("workload:", describe(cfg))
-    if args.discover:
+    if args.precompute:
+        if "--steps" not in sys.argv:
+            args.steps = 5
+        if "--warmup" not in sys.argv:
+            args.warmup = 1
+        result = run_precompute(args, cfg)
+    elif args.discover:
         result = run_discover(args, cfg)
     elif args.tag:
         result = run_tag(args, cfg)

@@ -46,32 +46,51 @@ __device__ __forceinline__ float wave_sum(float v) {
 // ---------------------------------------------------------------- sorting --
 
 // Length histogram (counts[0..7]); lengths outside [2, max_len] raise ELEN.
+// Counts are summed per workgroup in LDS first, so each workgroup adds at
+// most one value per length to the global counters.
 __global__ __launch_bounds__(kThreads) void k_len_count(const int32_t* __restrict__ lengths,
                                                         int64_t n, int max_len,
                                                         unsigned* __restrict__ counts,
                                                         unsigned* __restrict__ status) {
+    __shared__ unsigned s_cnt[8];
+    if (threadIdx.x < 8) s_cnt[threadIdx.x] = 0;
+    __syncthreads();
     const int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (g >= n) return;
-    const int32_t L = lengths[g];
-    if (L < 2 || L > max_len) {
-        atomicOr(status, err_bit(SCONE_ELEN));
-        return;
+    if (g < n) {
+        const int32_t L = lengths[g];
+        if (L < 2 || L > max_len)
+            atomicOr(status, err_bit(SCONE_ELEN));
+        else
+            atomicAdd(s_cnt + L, 1u);
     }
-    atomicAdd(counts + L, 1u);
+    __syncthreads();
+    if (threadIdx.x < 8 && s_cnt[threadIdx.x]) atomicAdd(counts + threadIdx.x, s_cnt[threadIdx.x]);
 }
 
-// order[base[L] + k] = g for the f-grams of length L (any order inside a bucket).
+// order[base[L] + k] = g for the f-grams of length L (any order inside a
+// bucket).  A workgroup ranks its f-grams per length in LDS and reserves each
+// length's run with one global atomic.
 __global__ __launch_bounds__(kThreads) void k_len_scatter(const int32_t* __restrict__ lengths,
                                                           int64_t n, int max_len,
                                                           const int64_t* __restrict__ base,
                                                           unsigned* __restrict__ cursor,
                                                           int32_t* __restrict__ order) {
+    __shared__ unsigned s_cnt[8], s_off[8];
+    if (threadIdx.x < 8) s_cnt[threadIdx.x] = 0;
+    __syncthreads();
     const int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (g >= n) return;
-    const int32_t L = lengths[g];
-    if (L < 2 || L > max_len) return;
-    const unsigned k = atomicAdd(cursor + L, 1u);
-    order[base[L] + k] = (int32_t)g;
+    int32_t L = 0;
+    unsigned rank = 0;
+    if (g < n) {
+        L = lengths[g];
+        if (L >= 2 && L <= max_len) rank = atomicAdd(s_cnt + L, 1u);
+        else L = 0;
+    }
+    __syncthreads();
+    if (threadIdx.x < 8 && s_cnt[threadIdx.x])
+        s_off[threadIdx.x] = atomicAdd(cursor + threadIdx.x, s_cnt[threadIdx.x]);
+    __syncthreads();
+    if (L) order[base[L] + s_off[L] + rank] = (int32_t)g;
 }
 
 // -------------------------------------------------------------- row kernels --
@@ -497,9 +516,11 @@ extern "C" int scone_fgram_model_forward(const int32_t* fgrams, const int32_t* l
     Buffers B{};
     if (rc == SCONE_OK) {
         const size_t h_bytes = (size_t)align_up(ctok * d) * 4;
-        const size_t a_bytes = (size_t)align_up(ctok * d) * 2;
+        // matrix-product inputs (a, f) are readable up to a whole 256-row tile
+        const int64_t ptok = (ctok + 255) / 256 * 256;
+        const size_t a_bytes = (size_t)align_up(ptok * d) * 2;
         const size_t qkv_bytes = (size_t)align_up(ctok * 3 * d) * 2;
-        const size_t f_bytes = (size_t)align_up(ctok * d_ff) * 2;
+        const size_t f_bytes = (size_t)align_up(ptok * d_ff) * 2;
         if (hipMalloc(&act, h_bytes + a_bytes + qkv_bytes + f_bytes) != hipSuccess) {
             act = nullptr;
             fail(SCONE_ENOMEM);

@@ -6,16 +6,23 @@
 //   kGelu:  out_bf16[m, n]  = bf16(GELU(C))             (exact, erf form)
 //   kResid: out_f32[m, n]  += C                         (the residual stream)
 //
-// Both operands are K-contiguous, so every tile row is a run of 16-byte
-// loads.  A workgroup of four wavefronts computes a 128 x 128 tile with a
-// 64-deep k-slab double-buffered in LDS (one barrier per slab).  Each
-// wavefront owns a 64 x 64 quarter as 4 x 4 v_mfma_f32_16x16x32_bf16 tiles.
-// W is passed as the instruction's first operand and A as the second, so a
-// lane's four accumulators are four consecutive n of one row m: the epilogue
-// writes 8 bytes (bf16) or 16 bytes (f32) per lane per tile.
+// Both operands are K-contiguous.  A workgroup computes a BM x BN tile over
+// 64-deep k-slabs held in a two-stage LDS ring.  Slabs move from global
+// memory straight into LDS (global_load_lds_dwordx4: no registers, no LDS
+// write instructions); the next slab is in flight while the current one is
+// multiplied, and the only synchronisation per slab is a counted wait on the
+// wavefront's own copies plus a workgroup barrier.  Each wavefront owns a
+// (BM / WGM) x (BN / WGN) part of the tile as 16 x 16 v_mfma_f32_16x16x32_bf16
+// tiles.  W is the instruction's first operand and A the second, so a lane's
+// four accumulators are four consecutive n of one row m: the epilogue writes
+// 8 bytes (bf16) or 16 bytes (f32) per lane per tile.
 //
-// LDS rows are padded from 64 to 72 elements (144 bytes), which spreads the
-// sixteen rows a fragment read touches over distinct banks.
+// LDS layout: a slab row is 64 elements = 128 bytes = eight 16-byte chunks,
+// stored at slot chunk ^ f(row) with f(r) = (r & 7) ^ ((r >> 3) & 1).  A
+// fragment read touches 16 consecutive rows (a multiple of 16 first) at one
+// chunk; the swizzle puts them in distinct banks whether the LDS serves 8 or
+// 16 lanes of a 16-byte read per cycle.  One copy instruction fills 1 KB of
+// LDS (8 whole rows), each lane fetching the chunk its slot must hold.
 #pragma once
 
 #include "scone_internal.h"
@@ -25,12 +32,8 @@ namespace gemm {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-constexpr int kThreads = 256;
-constexpr int kBM = 128;  // rows of A (tokens) per tile
-constexpr int kBN = 128;  // rows of W (output features) per tile
-constexpr int kBK = 64;   // k-slab
-constexpr int kLd = kBK + 8;  // padded LDS row, elements
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(1))) void* gbl_ptr_t;
 
 enum Epilogue { kBias = 0, kGelu = 1, kResid = 2 };
 
@@ -46,14 +49,30 @@ __device__ __forceinline__ float gelu_erf(float x) {
     return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
 }
 
-template <int EPI>
-__global__ __launch_bounds__(kThreads) void k_gemm(const uint16_t* __restrict__ A,
-                                                   const uint16_t* __restrict__ W,
-                                                   const uint16_t* __restrict__ bias,
-                                                   void* __restrict__ out, int M, int N, int K,
-                                                   int tiles_n) {
-    __shared__ __attribute__((aligned(16))) uint16_t sA[2][kBM * kLd];
-    __shared__ __attribute__((aligned(16))) uint16_t sW[2][kBN * kLd];
+// s_waitcnt immediates (gfx9 encoding): wait until at most n vector-memory
+// operations are outstanding / until no LDS operation is outstanding.
+constexpr int waitcnt_vm(int n) {
+    return (n & 0xF) | (7 << 4) | (0xF << 8) | (((n >> 4) & 3) << 14);
+}
+constexpr int kWaitLds = 0xF | (7 << 4) | (0 << 8) | (3 << 14);
+
+constexpr int kBK = 64;        // k-slab depth (elements)
+constexpr int kRowBytes = 128;  // one slab row in LDS
+
+template <int EPI, int BM, int BN, int WGM, int WGN>
+__global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restrict__ A,
+                                                         const uint16_t* __restrict__ W,
+                                                         const uint16_t* __restrict__ bias,
+                                                         void* __restrict__ out, int M, int N,
+                                                         int K, int tiles_n) {
+    constexpr int NW = WGM * WGN;
+    constexpr int WTM = BM / WGM, WTN = BN / WGN;  // wavefront tile
+    constexpr int TM = WTM / 16, TN = WTN / 16;
+    constexpr int STAGE = (BM + BN) * kRowBytes;
+    constexpr int GA = BM / 8 / NW, GW = BN / 8 / NW;  // 8-row copy groups per wavefront
+    static_assert(GA * 8 * NW == BM && GW * 8 * NW == BN && GA % 2 == 0 && GW % 2 == 0,
+                  "copy groups must split evenly and in pairs");
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * STAGE];
 
     // Consecutive workgroups land on different XCDs; renumber so that each
     // XCD walks a contiguous run of tiles (n fastest), which keeps the A rows
@@ -63,97 +82,95 @@ __global__ __launch_bounds__(kThreads) void k_gemm(const uint16_t* __restrict__ 
     const int per = nb / 8;
     const int t = (b < per * 8) ? (b % 8) * per + b / 8 : b;
     const int tm = t / tiles_n, tn = t % tiles_n;
-    const int m0 = tm * kBM, n0 = tn * kBN;
+    const int m0 = tm * BM, n0 = tn * BN;
 
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = wave / WGN, wn = wave % WGN;
 
-    // Global -> LDS copy: 256 threads x 16 bytes = 32 rows of 64 elements per pass.
-    const int lr = tid >> 3;         // 0..31
-    const int lc = (tid & 7) * 8;    // element column within the slab
-    const uint16_t* gA[4];
-    const uint16_t* gW[4];
-#pragma unroll
-    for (int p = 0; p < 4; ++p) {
-        int ra = m0 + lr + 32 * p;
-        ra = ra < M ? ra : M - 1;  // rows past M repeat the last row; never stored
-        gA[p] = A + (int64_t)ra * K + lc;
-        gW[p] = W + (int64_t)(n0 + lr + 32 * p) * K + lc;
-    }
+    // Copies: wavefront w fills 8-row groups w*GA .. w*GA+GA-1 of the A tile
+    // and w*GW .. of the W tile.  Lane l covers row l/8 of a group and slot
+    // l%8, which holds chunk (l%8) ^ f(row); f(8g + l/8) = (l/8) ^ (g & 1)
+    // and the first group of every wavefront is even.
+    const int lrow = lane >> 3, lslot = lane & 7;
+    const int c_even = (lslot ^ lrow) * 8, c_odd = (lslot ^ lrow ^ 1) * 8;
+    const int gA0 = wave * GA, gW0 = wave * GW;
+    // A has readable rows up to the next multiple of BM (rows past M hold
+    // anything: they only feed output rows that are never stored).
+    const uint16_t* pA = A + (int64_t)(m0 + gA0 * 8 + lrow) * K;
+    const uint16_t* pW = W + (int64_t)(n0 + gW0 * 8 + lrow) * K;
+    const int64_t grp = (int64_t)8 * K;
 
-    f32x4 acc[4][4];
+    auto issue = [&](int slab, int stage) {
+        const int ko = slab * kBK;
+        uint8_t* sbase = smem + stage * STAGE;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+        for (int j = 0; j < GA; ++j)
+            __builtin_amdgcn_global_load_lds(
+                (gbl_ptr_t)(pA + j * grp + ko + ((j & 1) ? c_odd : c_even)),
+                (lds_ptr_t)(sbase + (gA0 + j) * 1024), 16, 0, 0);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int j = 0; j < GW; ++j)
+            __builtin_amdgcn_global_load_lds(
+                (gbl_ptr_t)(pW + j * grp + ko + ((j & 1) ? c_odd : c_even)),
+                (lds_ptr_t)(sbase + BM * kRowBytes + (gW0 + j) * 1024), 16, 0, 0);
+    };
 
-    u32x4 ra[4], rw[4];
+    f32x4 acc[TN][TM];
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-        ra[p] = *reinterpret_cast<const u32x4*>(gA[p]);
-        rw[p] = *reinterpret_cast<const u32x4*>(gW[p]);
-    }
+    for (int i = 0; i < TN; ++i)
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-        *reinterpret_cast<u32x4*>(&sA[0][(lr + 32 * p) * kLd + lc]) = ra[p];
-        *reinterpret_cast<u32x4*>(&sW[0][(lr + 32 * p) * kLd + lc]) = rw[p];
-    }
-    __syncthreads();
+        for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int fr = lane & 15;         // fragment row
-    const int fk = (lane >> 4) * 8;   // fragment k offset
     const int KT = K / kBK;
+    issue(0, 0);
+    const int fr = lane & 15;                          // fragment row
+    const int swz = (lane & 7) ^ ((lane >> 3) & 1);    // f(fragment row)
+    const int q0 = lane >> 4;                          // fragment k chunk
     for (int kt = 0; kt < KT; ++kt) {
-        const int cur = kt & 1;
-        const bool more = kt + 1 < KT;
-        if (more) {
-            const int off = (kt + 1) * kBK;
+        // Slab kt is this wavefront's only outstanding copy; after the
+        // barrier every wavefront's part of it is in LDS, and every
+        // wavefront has finished reading the other stage.
+        __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+        __builtin_amdgcn_s_barrier();
+        if (kt + 1 < KT) issue(kt + 1, (kt + 1) & 1);
+        const uint8_t* sA = smem + (kt & 1) * STAGE;
+        const uint8_t* sW = sA + BM * kRowBytes;
 #pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                ra[p] = *reinterpret_cast<const u32x4*>(gA[p] + off);
-                rw[p] = *reinterpret_cast<const u32x4*>(gW[p] + off);
-            }
-        }
+        for (int ks = 0; ks < 2; ++ks) {
+            const int slot = ((ks * 4 + q0) ^ swz) * 16;
+            bf16x8 fw[TN], fa[TM];
 #pragma unroll
-        for (int ks = 0; ks < kBK; ks += 32) {
-            bf16x8 fw[4], fa[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < TN; ++i)
                 fw[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                    &sW[cur][(wn * 64 + i * 16 + fr) * kLd + ks + fk]));
-                fa[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                    &sA[cur][(wm * 64 + i * 16 + fr) * kLd + ks + fk]));
-            }
+                    sW + (wn * WTN + i * 16 + fr) * kRowBytes + slot));
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int j = 0; j < TM; ++j)
+                fa[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
+                    sA + (wm * WTM + j * 16 + fr) * kRowBytes + slot));
 #pragma unroll
-                for (int j = 0; j < 4; ++j)
+            for (int i = 0; i < TN; ++i)
+#pragma unroll
+                for (int j = 0; j < TM; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[i], fa[j], acc[i][j],
                                                                         0, 0, 0);
         }
-        if (more) {
-#pragma unroll
-            for (int p = 0; p < 4; ++p) {
-                *reinterpret_cast<u32x4*>(&sA[cur ^ 1][(lr + 32 * p) * kLd + lc]) = ra[p];
-                *reinterpret_cast<u32x4*>(&sW[cur ^ 1][(lr + 32 * p) * kLd + lc]) = rw[p];
-            }
-        }
-        __syncthreads();
+        // this stage's reads are done before any wavefront passes the next
+        // barrier and refills it
+        __builtin_amdgcn_s_waitcnt(kWaitLds);
     }
 
-    // acc[i][j][r] = C[m, n] with n = n0 + wn*64 + i*16 + (lane/16)*4 + r and
-    // m = m0 + wm*64 + j*16 + lane%16.
+    // acc[i][j][r] = C[m, n] with n = n0 + wn*WTN + i*16 + (lane/16)*4 + r and
+    // m = m0 + wm*WTM + j*16 + lane%16.
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int n = n0 + wn * 64 + i * 16 + (lane >> 4) * 4;
+    for (int i = 0; i < TN; ++i) {
+        const int n = n0 + wn * WTN + i * 16 + (lane >> 4) * 4;
         const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + n);
         const float b0 = bf16_to_f32(bb.x & 0xFFFFu), b1 = bf16_to_f32(bb.x >> 16);
         const float b2 = bf16_to_f32(bb.y & 0xFFFFu), b3 = bf16_to_f32(bb.y >> 16);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int m = m0 + wm * 64 + j * 16 + (lane & 15);
+        for (int j = 0; j < TM; ++j) {
+            const int m = m0 + wm * WTM + j * 16 + (lane & 15);
             if (m >= M) continue;
             float v0 = acc[i][j][0] + b0, v1 = acc[i][j][1] + b1;
             float v2 = acc[i][j][2] + b2, v3 = acc[i][j][3] + b3;
@@ -175,15 +192,27 @@ __global__ __launch_bounds__(kThreads) void k_gemm(const uint16_t* __restrict__ 
     }
 }
 
-// Shapes: N % 128 == 0, K % 64 == 0, M >= 1; all pointers 16-byte aligned.
+template <int EPI, int BM, int BN, int WGM, int WGN>
+inline hipError_t launch_tiles(const uint16_t* A, const uint16_t* W, const uint16_t* bias,
+                               void* out, int M, int N, int K, hipStream_t st) {
+    const int tiles_n = N / BN;
+    const int tiles_m = (M + BM - 1) / BM;
+    hipLaunchKernelGGL((k_gemm<EPI, BM, BN, WGM, WGN>), dim3((unsigned)(tiles_m * tiles_n)),
+                       dim3(64 * WGM * WGN), 0, st, A, W, bias, out, M, N, K, tiles_n);
+    return hipGetLastError();
+}
+
+// Shapes: N % 128 == 0, K % 64 == 0, M >= 1; all pointers 16-byte aligned;
+// A readable up to row roundup(M, 256).  Large products take 256 x 256 tiles
+// on eight wavefronts (half the LDS and L2 traffic per flop of 128 x 128);
+// N not a multiple of 256, or too few tiles to fill the 256 compute units,
+// take 128 x 128 on four.
 template <int EPI>
 inline hipError_t launch(const uint16_t* A, const uint16_t* W, const uint16_t* bias, void* out,
                          int M, int N, int K, hipStream_t st) {
-    const int tiles_n = N / kBN;
-    const int tiles_m = (M + kBM - 1) / kBM;
-    hipLaunchKernelGGL(k_gemm<EPI>, dim3((unsigned)(tiles_m * tiles_n)), dim3(kThreads), 0, st,
-                       A, W, bias, out, M, N, K, tiles_n);
-    return hipGetLastError();
+    if (N % 256 == 0 && (int64_t)((M + 255) / 256) * (N / 256) >= 256)
+        return launch_tiles<EPI, 256, 256, 2, 4>(A, W, bias, out, M, N, K, st);
+    return launch_tiles<EPI, 128, 128, 2, 2>(A, W, bias, out, M, N, K, st);
 }
 
 }  // namespace gemm
