@@ -700,13 +700,18 @@ def run_discover(args, cfg):
 
 
 def fgram_model_flops(lengths: np.ndarray, d: int, d_ff: int, n_layers: int) -> float:
-    """Algorithmic flops of the f-gram model over f-grams of these lengths: per
-    token and layer 2 (3d^2 + d^2 + 2 d d_ff) for the four products, and
-    4 (i + 1) d for the scores and the weighted sum of position i."""
+    """Algorithmic flops of precomputing F for f-grams of these lengths.  A
+    full layer costs, per token, 2 (3d^2 + d^2 + 2 d d_ff) for its four
+    products and 4 (i + 1) d for position i's scores and weighted sum.  F
+    needs only the last token's output, so the last layer computes q, k, v
+    for every token but attention, the output projection and the MLP for the
+    last position alone."""
+    if n_layers == 0:
+        return 0.0
     n = lengths.astype(np.float64)
-    tokens = n.sum()
-    attn_per_layer = (4.0 * d * n * (n + 1) / 2).sum()
-    return n_layers * (tokens * 2.0 * (4.0 * d * d + 2.0 * d * d_ff) + attn_per_layer)
+    full = n * 2.0 * (4.0 * d * d + 2.0 * d * d_ff) + 4.0 * d * n * (n + 1) / 2
+    last = n * 2.0 * 3.0 * d * d + 2.0 * (d * d + 2.0 * d * d_ff) + 4.0 * d * n
+    return float((n_layers - 1) * full.sum() + last.sum())
 
 
 def run_precompute(args, cfg):

@@ -168,9 +168,11 @@ __global__ __launch_bounds__(kThreads) void k_embed_ln(
     layer_norm_store<R>(x, g, b, lane, a + r * d);
 }
 
+// a[r] = LN(h + r * ld) for r < rows (ld = d, or n * d to take every f-gram's
+// last token from h + (n - 1) * d).
 template <int R>
 __global__ __launch_bounds__(kThreads) void k_ln(const float* __restrict__ h, int64_t rows,
-                                                 const uint16_t* __restrict__ g,
+                                                 int64_t ld, const uint16_t* __restrict__ g,
                                                  const uint16_t* __restrict__ b,
                                                  uint16_t* __restrict__ a) {
     constexpr int d = 256 * R;
@@ -180,7 +182,7 @@ __global__ __launch_bounds__(kThreads) void k_ln(const float* __restrict__ h, in
     float x[R][4];
 #pragma unroll
     for (int c = 0; c < R; ++c) {
-        const float4 v = *reinterpret_cast<const float4*>(h + r * d + c * 256 + lane * 4);
+        const float4 v = *reinterpret_cast<const float4*>(h + r * ld + c * 256 + lane * 4);
         x[c][0] = v.x; x[c][1] = v.y; x[c][2] = v.z; x[c][3] = v.w;
     }
     layer_norm_store<R>(x, g, b, lane, a + r * d);
@@ -221,7 +223,9 @@ __global__ __launch_bounds__(kThreads) void k_final(const float* __restrict__ h,
 // model: lane holds 8 consecutive columns, so a head of dh columns spans
 // dh / 8 lanes and its dot products are reduced over that many lanes.
 // qkv row r = [q | k | v], each d wide; o row r = concatenated heads.
-template <int LPH, int N>  // lanes per head (dh / 8), f-gram length
+// kLast: only the last position's output, written to o row f (the last
+// layer needs nothing else).
+template <int LPH, int N, bool kLast>  // lanes per head (dh / 8), f-gram length
 __global__ __launch_bounds__(kThreads) void k_attn(const uint16_t* __restrict__ qkv,
                                                    uint16_t* __restrict__ o, int64_t n_f, int d,
                                                    float scale) {
@@ -241,7 +245,7 @@ __global__ __launch_bounds__(kThreads) void k_attn(const uint16_t* __restrict__ 
             vv[j] = *reinterpret_cast<const u32x4*>(row + 2 * d);
         }
 #pragma unroll
-        for (int i = 0; i < N; ++i) {
+        for (int i = kLast ? N - 1 : 0; i < N; ++i) {
             float s[N];
             float mx = -3.0e38f;
 #pragma unroll
@@ -278,25 +282,39 @@ __global__ __launch_bounds__(kThreads) void k_attn(const uint16_t* __restrict__ 
 #pragma unroll
             for (int e = 0; e < 4; ++e)
                 ov[e] = f32_to_bf16(acc[2 * e]) | (f32_to_bf16(acc[2 * e + 1]) << 16);
-            *reinterpret_cast<u32x4*>(o + (r0 + i) * (int64_t)d + col) = ov;
+            *reinterpret_cast<u32x4*>(o + (kLast ? f : r0 + i) * (int64_t)d + col) = ov;
         }
     }
 }
 
-template <int LPH>
+template <int LPH, bool kLast>
 hipError_t launch_attn(const uint16_t* qkv, uint16_t* o, int64_t n_f, int n, int d, float scale,
                        hipStream_t st) {
     const dim3 grid((unsigned)((n_f + 3) / 4)), block(kThreads);
     switch (n) {
-        case 2: hipLaunchKernelGGL((k_attn<LPH, 2>), grid, block, 0, st, qkv, o, n_f, d, scale); break;
-        case 3: hipLaunchKernelGGL((k_attn<LPH, 3>), grid, block, 0, st, qkv, o, n_f, d, scale); break;
-        case 4: hipLaunchKernelGGL((k_attn<LPH, 4>), grid, block, 0, st, qkv, o, n_f, d, scale); break;
-        case 5: hipLaunchKernelGGL((k_attn<LPH, 5>), grid, block, 0, st, qkv, o, n_f, d, scale); break;
-        case 6: hipLaunchKernelGGL((k_attn<LPH, 6>), grid, block, 0, st, qkv, o, n_f, d, scale); break;
-        case 7: hipLaunchKernelGGL((k_attn<LPH, 7>), grid, block, 0, st, qkv, o, n_f, d, scale); break;
+#define SCONE_ATTN_CASE(NN)                                                                  \
+    case NN:                                                                                 \
+        hipLaunchKernelGGL((k_attn<LPH, NN, kLast>), grid, block, 0, st, qkv, o, n_f, d, scale); \
+        break;
+        SCONE_ATTN_CASE(2)
+        SCONE_ATTN_CASE(3)
+        SCONE_ATTN_CASE(4)
+        SCONE_ATTN_CASE(5)
+        SCONE_ATTN_CASE(6)
+        SCONE_ATTN_CASE(7)
+#undef SCONE_ATTN_CASE
         default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
+}
+
+hipError_t attention(const uint16_t* qkv, uint16_t* o, int64_t n_f, int n, int d, int dh,
+                     bool last, float scale, hipStream_t st) {
+    if (dh == 64)
+        return last ? launch_attn<8, true>(qkv, o, n_f, n, d, scale, st)
+                    : launch_attn<8, false>(qkv, o, n_f, n, d, scale, st);
+    return last ? launch_attn<16, true>(qkv, o, n_f, n, d, scale, st)
+                : launch_attn<16, false>(qkv, o, n_f, n, d, scale, st);
 }
 
 // ------------------------------------------------------------------ layout --
@@ -390,21 +408,28 @@ hipError_t run_chunk(const Weights& w, const int32_t* order, int64_t n_f, int n,
     for (int l = 0; l < n_layers && e == hipSuccess; ++l) {
         const Weights::Layer& L = w.layers[l];
         if (l > 0)
-            hipLaunchKernelGGL(k_ln<R>, dim3(g_rows), dim3(kThreads), 0, st, B.h, M, L.ln1_g,
-                               L.ln1_b, B.a);
-        e = gemm::launch<gemm::kBias>(B.a, L.w_qkv, L.b_qkv, B.qkv, (int)M, 3 * d, d, st);
+            hipLaunchKernelGGL(k_ln<R>, dim3(g_rows), dim3(kThreads), 0, st, B.h, M, (int64_t)d,
+                               L.ln1_g, L.ln1_b, B.a);
+        e = gemm::launch<gemm::kBias>(B.a, L.w_qkv, L.b_qkv, B.qkv, 3 * d, (int)M, 3 * d, d, st);
         if (e != hipSuccess) break;
+        // Only the last token's state reaches F, so after the last layer's
+        // attention every product runs on one row per f-gram: rows of h are
+        // then taken with stride n * d from the last position.
+        const bool last = l == n_layers - 1;
+        const int64_t Mr = last ? n_f : M;
+        float* hr = last ? B.h + (int64_t)(n - 1) * d : B.h;
+        const int64_t ldh = last ? (int64_t)n * d : d;
+        const unsigned g_r = (unsigned)((Mr + 3) / 4);
         // attention output overwrites a (its input to the qkv product is consumed)
-        e = dh == 64 ? launch_attn<8>(B.qkv, B.a, n_f, n, d, scale, st)
-                     : launch_attn<16>(B.qkv, B.a, n_f, n, d, scale, st);
+        e = attention(B.qkv, B.a, n_f, n, d, dh, last, scale, st);
         if (e != hipSuccess) break;
-        e = gemm::launch<gemm::kResid>(B.a, L.w_o, L.b_o, B.h, (int)M, d, d, st);
+        e = gemm::launch<gemm::kResid>(B.a, L.w_o, L.b_o, hr, ldh, (int)Mr, d, d, st);
         if (e != hipSuccess) break;
-        hipLaunchKernelGGL(k_ln<R>, dim3(g_rows), dim3(kThreads), 0, st, B.h, M, L.ln2_g,
+        hipLaunchKernelGGL(k_ln<R>, dim3(g_r), dim3(kThreads), 0, st, hr, Mr, ldh, L.ln2_g,
                            L.ln2_b, B.a);
-        e = gemm::launch<gemm::kGelu>(B.a, L.w_fc1, L.b_fc1, B.f, (int)M, d_ff, d, st);
+        e = gemm::launch<gemm::kGelu>(B.a, L.w_fc1, L.b_fc1, B.f, d_ff, (int)Mr, d_ff, d, st);
         if (e != hipSuccess) break;
-        e = gemm::launch<gemm::kResid>(B.f, L.w_fc2, L.b_fc2, B.h, (int)M, d, d_ff, st);
+        e = gemm::launch<gemm::kResid>(B.f, L.w_fc2, L.b_fc2, hr, ldh, (int)Mr, d, d_ff, st);
     }
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_final<R>, dim3(g_f), dim3(kThreads), 0, st, B.h, order, n_f, n, row_ids,

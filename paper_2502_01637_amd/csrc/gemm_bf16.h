@@ -63,8 +63,8 @@ template <int EPI, int BM, int BN, int WGM, int WGN>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restrict__ A,
                                                          const uint16_t* __restrict__ W,
                                                          const uint16_t* __restrict__ bias,
-                                                         void* __restrict__ out, int M, int N,
-                                                         int K, int tiles_n) {
+                                                         void* __restrict__ out, int64_t ldc,
+                                                         int M, int N, int K, int tiles_n) {
     constexpr int NW = WGM * WGN;
     constexpr int WTM = BM / WGM, WTN = BN / WGN;  // wavefront tile
     constexpr int TM = WTM / 16, TN = WTN / 16;
@@ -175,7 +175,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
             float v0 = acc[i][j][0] + b0, v1 = acc[i][j][1] + b1;
             float v2 = acc[i][j][2] + b2, v3 = acc[i][j][3] + b3;
             if (EPI == kResid) {
-                f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(out) + (int64_t)m * N + n);
+                f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(out) + m * ldc + n);
                 f32x4 h = *p;
                 h[0] += v0; h[1] += v1; h[2] += v2; h[3] += v3;
                 *p = h;
@@ -186,7 +186,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
                 u32x2 o;
                 o.x = f32_to_bf16(v0) | (f32_to_bf16(v1) << 16);
                 o.y = f32_to_bf16(v2) | (f32_to_bf16(v3) << 16);
-                *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(out) + (int64_t)m * N + n) = o;
+                *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(out) + m * ldc + n) = o;
             }
         }
     }
@@ -194,25 +194,26 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
 
 template <int EPI, int BM, int BN, int WGM, int WGN>
 inline hipError_t launch_tiles(const uint16_t* A, const uint16_t* W, const uint16_t* bias,
-                               void* out, int M, int N, int K, hipStream_t st) {
+                               void* out, int64_t ldc, int M, int N, int K, hipStream_t st) {
     const int tiles_n = N / BN;
     const int tiles_m = (M + BM - 1) / BM;
     hipLaunchKernelGGL((k_gemm<EPI, BM, BN, WGM, WGN>), dim3((unsigned)(tiles_m * tiles_n)),
-                       dim3(64 * WGM * WGN), 0, st, A, W, bias, out, M, N, K, tiles_n);
+                       dim3(64 * WGM * WGN), 0, st, A, W, bias, out, ldc, M, N, K, tiles_n);
     return hipGetLastError();
 }
 
 // Shapes: N % 128 == 0, K % 64 == 0, M >= 1; all pointers 16-byte aligned;
-// A readable up to row roundup(M, 256).  Large products take 256 x 256 tiles
+// A readable up to row roundup(M, 256); output row m starts at out + m * ldc
+// elements (ldc >= N, a multiple of 4).  Large products take 256 x 256 tiles
 // on eight wavefronts (half the LDS and L2 traffic per flop of 128 x 128);
 // N not a multiple of 256, or too few tiles to fill the 256 compute units,
 // take 128 x 128 on four.
 template <int EPI>
 inline hipError_t launch(const uint16_t* A, const uint16_t* W, const uint16_t* bias, void* out,
-                         int M, int N, int K, hipStream_t st) {
+                         int64_t ldc, int M, int N, int K, hipStream_t st) {
     if (N % 256 == 0 && (int64_t)((M + 255) / 256) * (N / 256) >= 256)
-        return launch_tiles<EPI, 256, 256, 2, 4>(A, W, bias, out, M, N, K, st);
-    return launch_tiles<EPI, 128, 128, 2, 2>(A, W, bias, out, M, N, K, st);
+        return launch_tiles<EPI, 256, 256, 2, 4>(A, W, bias, out, ldc, M, N, K, st);
+    return launch_tiles<EPI, 128, 128, 2, 2>(A, W, bias, out, ldc, M, N, K, st);
 }
 
 }  // namespace gemm
