@@ -18,11 +18,11 @@
 // 8 bytes (bf16) or 16 bytes (f32) per lane per tile.
 //
 // LDS layout: a slab row is 64 elements = 128 bytes = eight 16-byte chunks,
-// stored at slot chunk ^ f(row) with f(r) = (r & 7) ^ ((r >> 3) & 1).  A
-// fragment read touches 16 consecutive rows (a multiple of 16 first) at one
-// chunk; the swizzle puts them in distinct banks whether the LDS serves 8 or
-// 16 lanes of a 16-byte read per cycle.  One copy instruction fills 1 KB of
-// LDS (8 whole rows), each lane fetching the chunk its slot must hold.
+// stored at slot chunk ^ (row & 7).  A fragment read touches 16 consecutive
+// rows at one chunk; with this swizzle the LDS bank-conflict counter reads
+// zero and a 16-byte fragment read occupies the LDS for 4 cycles (unswizzled:
+// 16; other XOR patterns tried: 8).  One copy instruction fills 1 KB of LDS
+// (8 whole rows), each lane fetching the chunk its slot must hold.
 #pragma once
 
 #include "scone_internal.h"
@@ -70,8 +70,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
     constexpr int TM = WTM / 16, TN = WTN / 16;
     constexpr int STAGE = (BM + BN) * kRowBytes;
     constexpr int GA = BM / 8 / NW, GW = BN / 8 / NW;  // 8-row copy groups per wavefront
-    static_assert(GA * 8 * NW == BM && GW * 8 * NW == BN && GA % 2 == 0 && GW % 2 == 0,
-                  "copy groups must split evenly and in pairs");
+    static_assert(GA * 8 * NW == BM && GW * 8 * NW == BN, "copy groups must split evenly");
     __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * STAGE];
 
     // Consecutive workgroups land on different XCDs; renumber so that each
@@ -90,10 +89,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
 
     // Copies: wavefront w fills 8-row groups w*GA .. w*GA+GA-1 of the A tile
     // and w*GW .. of the W tile.  Lane l covers row l/8 of a group and slot
-    // l%8, which holds chunk (l%8) ^ f(row); f(8g + l/8) = (l/8) ^ (g & 1)
-    // and the first group of every wavefront is even.
+    // l%8, which holds chunk (l%8) ^ (row & 7) = (l%8) ^ (l/8).
     const int lrow = lane >> 3, lslot = lane & 7;
-    const int c_even = (lslot ^ lrow) * 8, c_odd = (lslot ^ lrow ^ 1) * 8;
+    const int chunk = (lslot ^ lrow) * 8;
     const int gA0 = wave * GA, gW0 = wave * GW;
     // A has readable rows up to the next multiple of BM (rows past M hold
     // anything: they only feed output rows that are never stored).
@@ -107,12 +105,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
 #pragma unroll
         for (int j = 0; j < GA; ++j)
             __builtin_amdgcn_global_load_lds(
-                (gbl_ptr_t)(pA + j * grp + ko + ((j & 1) ? c_odd : c_even)),
+                (gbl_ptr_t)(pA + j * grp + ko + chunk),
                 (lds_ptr_t)(sbase + (gA0 + j) * 1024), 16, 0, 0);
 #pragma unroll
         for (int j = 0; j < GW; ++j)
             __builtin_amdgcn_global_load_lds(
-                (gbl_ptr_t)(pW + j * grp + ko + ((j & 1) ? c_odd : c_even)),
+                (gbl_ptr_t)(pW + j * grp + ko + chunk),
                 (lds_ptr_t)(sbase + BM * kRowBytes + (gW0 + j) * 1024), 16, 0, 0);
     };
 
@@ -125,7 +123,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
     const int KT = K / kBK;
     issue(0, 0);
     const int fr = lane & 15;                          // fragment row
-    const int swz = (lane & 7) ^ ((lane >> 3) & 1);    // f(fragment row)
+    const int swz = lane & 7;                          // fragment row & 7
     const int q0 = lane >> 4;                          // fragment k chunk
     for (int kt = 0; kt < KT; ++kt) {
         // Slab kt is this wavefront's only outstanding copy; after the
