@@ -101,6 +101,23 @@ def test_forward_matches_oracle(cfg, N):
     assert not got[untouched].any()
 
 
+def test_tiny_and_empty_buckets():
+    """Buckets of 1, 2 and 3 f-grams (products with M < 16) next to empty
+    lengths; 128-wide heads so the attention takes its other lane grouping."""
+    cfg = ModelConfig(512, 4, 768, 2, 7)
+    rng = np.random.default_rng(10)
+    V = 200
+    P = make_params(cfg, seed=71)
+    T = make_token_rows(V, cfg.d, seed=72)
+    lengths = np.array([7, 2, 5, 5, 7, 5], dtype=np.int32)   # no 3, 4 or 6
+    fg, lengths = random_fgrams(rng, V, len(lengths), cfg.max_len, lengths)
+    ids = np.array([5, 0, 3, 1, 4, 2], dtype=np.int32)
+    got = as_f64(run(cfg, fg, lengths, ids, T, P, 6))
+    ref = orc.forward(fg, lengths, bf16_bits_to_f64(T),
+                      {k: bf16_bits_to_f64(v) for k, v in P.items()}, cfg.n_layers, cfg.n_heads)
+    assert_close(got[ids], ref, cfg.n_layers, "tiny buckets")
+
+
 def test_several_chunks_per_length():
     """More than 65536 tokens of one length: the bucket runs in several chunks."""
     cfg = ModelConfig(512, 8, 512, 1, 3)
