@@ -699,6 +699,16 @@ def run_discover(args, cfg):
     return result
 
 
+def blas_threads() -> int:
+    """Threads of numpy's BLAS pool (the oracle's matrix products run there)."""
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"]
+        return int(max(n)) if n else 1
+    except ImportError:
+        return 1
+
+
 def fgram_model_flops(lengths: np.ndarray, d: int, d_ff: int, n_layers: int) -> float:
     """Algorithmic flops of precomputing F for f-grams of these lengths.  A
     full layer costs, per token, 2 (3d^2 + d^2 + 2 d d_ff) for its four
@@ -790,7 +800,7 @@ def run_precompute(args, cfg):
                 break
         el = time.perf_counter() - t0
         result["cpu_baseline"] = {"value": reps * len(cs) / el, "unit": "f-grams/s",
-                                  "cores": torch.get_num_threads(), "kind": "oracle",
+                                  "cores": blas_threads(), "kind": "oracle",
                                   "sample": f"{len(cs)} f-grams, repeated {reps} times, "
                                             "float64 numpy (BLAS threads)"}
     return result
