@@ -159,32 +159,51 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
     }
 
     // acc[i][j][r] = C[m, n] with n = n0 + wn*WTN + i*16 + (lane/16)*4 + r and
-    // m = m0 + wm*WTM + j*16 + lane%16.
+    // m = m0 + wm*WTM + j*16 + lane%16.  Every load the epilogue needs (the
+    // biases, and for kResid a column group's residual values) is issued
+    // before its first use, so a wavefront waits once per group instead of
+    // once per 16 x 16 tile; rows past M read row M - 1 and are not stored.
+    u32x2 bb[TN];
+#pragma unroll
+    for (int i = 0; i < TN; ++i)
+        bb[i] = *reinterpret_cast<const u32x2*>(bias + n0 + wn * WTN + i * 16 + (lane >> 4) * 4);
 #pragma unroll
     for (int i = 0; i < TN; ++i) {
         const int n = n0 + wn * WTN + i * 16 + (lane >> 4) * 4;
-        const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + n);
-        const float b0 = bf16_to_f32(bb.x & 0xFFFFu), b1 = bf16_to_f32(bb.x >> 16);
-        const float b2 = bf16_to_f32(bb.y & 0xFFFFu), b3 = bf16_to_f32(bb.y >> 16);
+        const float b0 = bf16_to_f32(bb[i].x & 0xFFFFu), b1 = bf16_to_f32(bb[i].x >> 16);
+        const float b2 = bf16_to_f32(bb[i].y & 0xFFFFu), b3 = bf16_to_f32(bb[i].y >> 16);
+        if (EPI == kResid) {
+            float* o = static_cast<float*>(out);
+            f32x4 h[TM];
 #pragma unroll
-        for (int j = 0; j < TM; ++j) {
-            const int m = m0 + wm * WTM + j * 16 + (lane & 15);
-            if (m >= M) continue;
-            float v0 = acc[i][j][0] + b0, v1 = acc[i][j][1] + b1;
-            float v2 = acc[i][j][2] + b2, v3 = acc[i][j][3] + b3;
-            if (EPI == kResid) {
-                f32x4* p = reinterpret_cast<f32x4*>(static_cast<float*>(out) + m * ldc + n);
-                f32x4 h = *p;
-                h[0] += v0; h[1] += v1; h[2] += v2; h[3] += v3;
-                *p = h;
-            } else {
+            for (int j = 0; j < TM; ++j) {
+                const int m = m0 + wm * WTM + j * 16 + (lane & 15);
+                h[j] = *reinterpret_cast<const f32x4*>(o + (int64_t)(m < M ? m : M - 1) * ldc + n);
+            }
+#pragma unroll
+            for (int j = 0; j < TM; ++j) {
+                const int m = m0 + wm * WTM + j * 16 + (lane & 15);
+                if (m >= M) continue;
+                h[j][0] += acc[i][j][0] + b0;
+                h[j][1] += acc[i][j][1] + b1;
+                h[j][2] += acc[i][j][2] + b2;
+                h[j][3] += acc[i][j][3] + b3;
+                *reinterpret_cast<f32x4*>(o + (int64_t)m * ldc + n) = h[j];
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < TM; ++j) {
+                const int m = m0 + wm * WTM + j * 16 + (lane & 15);
+                if (m >= M) continue;
+                float v0 = acc[i][j][0] + b0, v1 = acc[i][j][1] + b1;
+                float v2 = acc[i][j][2] + b2, v3 = acc[i][j][3] + b3;
                 if (EPI == kGelu) {
                     v0 = gelu_erf(v0); v1 = gelu_erf(v1); v2 = gelu_erf(v2); v3 = gelu_erf(v3);
                 }
                 u32x2 o;
                 o.x = f32_to_bf16(v0) | (f32_to_bf16(v1) << 16);
                 o.y = f32_to_bf16(v2) | (f32_to_bf16(v3) << 16);
-                *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(out) + m * ldc + n) = o;
+                *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(out) + (int64_t)m * ldc + n) = o;
             }
         }
     }
