@@ -132,3 +132,91 @@ def test_decode_full_size():
         assert sampled_oracle_rows(cfg, rows, exp_ids[:, s], n=64, seed=s), s
     # the context after the last step holds each sequence's last max_n-1 tokens
     np.testing.assert_array_equal(ctx.cpu().numpy(), w.tokens[:, -(cfg.max_n - 1):])
+
+
+@pytest.fixture(scope="module")
+def c3_corpus():
+    cfg = CONFIGS["c3_10m_k5"]
+    w = make_workload(cfg)
+    return cfg, w, np.concatenate(query_batches(w, 128))
+
+
+def test_tag_full_size(c3_corpus):
+    """The tagger on 64 query batches of the K = 5 workload (8.4M tokens), as
+    bench.py --tag runs it: sampled rows against the oracle, the histogram
+    against the lengths."""
+    cfg, w, corpus = c3_corpus
+    X = corpus[:64 * cfg.B]
+    tb = build_gpu(w.fgrams, w.lengths, w.ids)
+    hist = torch.zeros(S.scone.MAX_FGRAM_LEN + 1, dtype=torch.int64, device="cuda")
+    ml, _ = S.tag(tb, dev(X), cfg.max_n, hist=hist)
+    S.check_ok()
+    ml = ml.cpu().numpy()
+    h = hist.cpu().numpy()
+    np.testing.assert_array_equal(h, np.bincount(ml.ravel(), minlength=len(h)))
+    rows = np.random.default_rng(3).choice(X.shape[0], 48, replace=False)
+    o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
+    _, exp_len = o.lookup(X[rows], cfg.max_n)
+    np.testing.assert_array_equal(ml[rows], exp_len)
+
+
+def _window_codes(X, n):
+    """Per window of n tokens (within rows): the last min(n, 4) tokens packed
+    16 bits each, and the first token (used when n = 5)."""
+    B, T = X.shape
+    x = X.astype(np.uint64)
+    m = min(n, 4)
+    code = np.zeros((B, T - n + 1), dtype=np.uint64)
+    for i in range(n - m, n):
+        code = (code << np.uint64(16)) | x[:, i:T - n + 1 + i]
+    return code.ravel(), x[:, 0:T - n + 1].ravel()
+
+
+def _count(codes, g):
+    n = len(g)
+    code, first = codes[n]
+    m = min(n, 4)
+    c = np.uint64(0)
+    for v in g[n - m:]:
+        c = (c << np.uint64(16)) | np.uint64(v)
+    hit = code == c
+    if n == 5:
+        hit &= first == np.uint64(g[0])
+    return int(hit.sum())
+
+
+def test_discovery_full_size(c3_corpus):
+    """Discovery on 128 query batches of the K = 5 workload (16.8M tokens),
+    S = 1M, minimum count 5, as bench.py --discover runs it.  Counting every
+    candidate on the CPU takes minutes, so the checks are sampled and exact:
+    returned counts equal direct counts in the corpus, and any sampled corpus
+    window counting more than the smallest kept count was kept."""
+    cfg, w, X = c3_corpus
+    K, Sn, mc = 5, 1_000_000, 5
+    fg, ln, ct = S.discover_fgrams(dev(X), K, Sn, mc)
+    fg, ln, ct = fg.cpu().numpy(), ln.cpu().numpy(), ct.cpu().numpy()
+    assert len(ln) == Sn                      # far more than 1M candidates exist
+    assert ((ln >= 2) & (ln <= K)).all()
+    for L in range(2, K + 1):
+        sel = ln == L
+        assert (fg[sel, :L] >= 0).all() and (fg[sel, L:] == -1).all()
+    assert (ct[ln >= 3] >= mc).all() and (ct >= 1).all()
+    keys = {tuple(int(v) for v in r[:L]) for r, L in zip(fg, ln)}
+    assert len(keys) == Sn
+    cmin = int(ct.min())
+    codes = {n: _window_codes(X, n) for n in range(2, K + 1)}
+    rng = np.random.default_rng(4)
+    for k in rng.choice(Sn, 40, replace=False):
+        g = tuple(int(v) for v in fg[k, :ln[k]])
+        assert _count(codes, g) == int(ct[k]), g
+    B, T = X.shape
+    for _ in range(120):
+        n = int(rng.integers(2, K + 1))
+        b, t = int(rng.integers(B)), int(rng.integers(n - 1, T))
+        g = tuple(int(v) for v in X[b, t - n + 1:t + 1])
+        c = _count(codes, g)
+        candidate = n == 2 or c >= mc      # Section 3.1: n >= 3 needs the minimum count
+        if candidate and c > cmin:
+            assert g in keys, (g, c, cmin)
+        if n >= 3 and c < mc:
+            assert g not in keys, (g, c)
