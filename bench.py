@@ -510,6 +510,41 @@ def run_decode(args, cfg):
     # events would dominate a step this short)
     step_us = min(graph_ev_ms) * 1e3 / steps
 
+    # Latency against batch size (the paper's inference study reports
+    # per-token embedding latency for batches of 1 to 16): the first sq
+    # sequences, 256 steps captured in a graph, device time per step.
+    sweep = []
+    st_n = min(steps, 256)
+    for sq in (1, 2, 4, 8, 16, 32, 64, 128, 256):
+        if sq > Sq:
+            break
+        Xq = Xs[:st_n, :sq].contiguous()
+        ctx_q = torch.zeros((sq, cap), dtype=torch.int32, device=dev)
+        clen_q = torch.zeros(sq, dtype=torch.int32, device=dev)
+        out_q = torch.empty((sq, cfg.d), dtype=E.dtype, device=dev)
+        ids_q = torch.empty((st_n, sq), dtype=torch.int32, device=dev)
+        gq = torch.cuda.CUDAGraph()
+        torch.cuda.synchronize()
+        with torch.cuda.graph(gq):
+            for s in range(st_n):
+                S.decode_step(table, ctx_q, clen_q, Xq[s], cfg.max_n, E, out_q,
+                              fgram_ids=ids_q[s])
+        ev_ms = []
+        for r in range(3):
+            clen_q.fill_(0)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            gq.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            ev_ms.append(e0.elapsed_time(e1))
+        if S.check() != 0 or not np.array_equal(ids_q.cpu().numpy(), ids_eager[:st_n, :sq]):
+            raise SystemExit(f"batch-size sweep at {sq} sequences differs from the eager decode")
+        us = min(ev_ms) * 1e3 / st_n
+        sweep.append({"sequences": sq, "us_per_step": us, "us_per_token": us / sq})
+        del gq
+
     tokens = Sq * steps
     per_step_bytes = Sq * (2 * cfg.row_bytes + 4)
     kernel_GBps = per_step_bytes / (step_us * 1e-6) / 1e9
@@ -542,6 +577,7 @@ def run_decode(args, cfg):
                      "note": "2.1 MB per step: launch-latency bound, not bandwidth bound"},
         "match": match_stats(lens.cpu().numpy(), cfg.max_n),
         "build_ms": build_s * 1e3,
+        "batch_sweep": sweep,
     }
     if not args.no_cpu_baseline:
         import oracle
