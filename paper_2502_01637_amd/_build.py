@@ -21,6 +21,19 @@ def command(out):
             + [os.path.join(CSRC, s) for s in SOURCES])
 
 
+EXAMPLE_SRC = os.path.join(PKG, "examples", "scone_embed.c")
+EXAMPLE = os.path.join(PKG, "examples", "scone_embed")
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+
+
+def example_command(out):
+    """The plain-C example: C99 with gcc, the HIP runtime and libscone.so only."""
+    return ["gcc", "-std=c99", "-O2", "-Wall", "-D__HIP_PLATFORM_AMD__",
+            "-I", os.path.join(ROCM, "include"), "-I", os.path.join(ROOT, "include"),
+            EXAMPLE_SRC, "-o", out, "-L", PKG, "-lscone", "-L", os.path.join(ROCM, "lib"),
+            "-lamdhip64", "-Wl,-rpath,$ORIGIN/..", "-Wl,-rpath," + os.path.join(ROCM, "lib")]
+
+
 def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = command(tmp)
@@ -28,6 +41,12 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)
     os.replace(tmp, LIB)
+    tmp = EXAMPLE + ".tmp%d" % os.getpid()
+    cmd = example_command(tmp)
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.check_call(cmd)
+    os.replace(tmp, EXAMPLE)
     return LIB
 
 
