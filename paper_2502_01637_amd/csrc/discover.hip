@@ -37,6 +37,13 @@ __device__ __forceinline__ uint64_t count_hash(uint64_t key) {
     return fmix64(key ^ 0x9E3779B97F4A7C15ULL);
 }
 
+// Candidate and survivor slots are claimed in chunks: a wavefront owns
+// kChunk consecutive entries, counts them in a first pass, reserves its whole
+// range with one atomic per counter, and fills it in a second pass.  (One
+// atomic per wavefront on a shared counter still serialises half a million
+// times per scan at these sizes.)
+constexpr int kChunk = 4096;
+
 __global__ __launch_bounds__(kThreads) void k_table_clear(CountSlot* __restrict__ t,
                                                           uint64_t cap) {
     const uint64_t i = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
@@ -100,23 +107,58 @@ __global__ __launch_bounds__(kThreads) void k_survivors(
     unsigned* __restrict__ n_surv, uint64_t* __restrict__ skey, unsigned* __restrict__ n_cand,
     uint64_t* __restrict__ cand_key, uint32_t* __restrict__ cand_count,
     int8_t* __restrict__ cand_level, unsigned* __restrict__ max_count) {
-    const uint64_t s = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (s >= cap) return;
-    const uint64_t key = t[s].key;
-    if (key == kEmptyKey) return;
-    const uint32_t c = t[s].count;
-    const bool survive = c >= min_count;
-    if (survive) {
-        const unsigned id = atomicAdd(n_surv, 1u);
-        t[s].dense = (int32_t)id;
-        if (skey) skey[id] = key;
+    const uint64_t s0 = ((uint64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6)) * kChunk;
+    if (s0 >= cap) return;  // wave-uniform
+    const uint64_t s1 = s0 + kChunk < cap ? s0 + kChunk : cap;
+    const int lane = threadIdx.x & 63;
+    const unsigned long long below = (1ull << lane) - 1ull;
+    unsigned ns = 0, nc = 0;
+    uint32_t mx = 0;
+    for (uint64_t b = s0; b < s1; b += 64) {
+        const uint64_t s = b + lane;
+        const uint64_t key = s < s1 ? t[s].key : kEmptyKey;
+        const bool occupied = key != kEmptyKey;
+        const uint32_t c = occupied ? t[s].count : 0;
+        const bool survive = occupied && c >= min_count;
+        const bool cand = occupied && (survive || keep_all);
+        ns += (unsigned)__popcll(__ballot(survive));
+        nc += (unsigned)__popcll(__ballot(cand));
+        if (cand) mx = c > mx ? c : mx;
     }
-    if (survive || keep_all) {
-        const unsigned k = atomicAdd(n_cand, 1u);
-        cand_key[k] = key;
-        cand_count[k] = c;
-        cand_level[k] = (int8_t)level;
-        atomicMax(max_count, c);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+        const uint32_t y = (uint32_t)__shfl_xor((int)mx, o);
+        mx = y > mx ? y : mx;
+    }
+    unsigned bs = 0, bc = 0;
+    if (lane == 0) {
+        if (ns) bs = atomicAdd(n_surv, ns);
+        if (nc) bc = atomicAdd(n_cand, nc);
+        if (mx) atomicMax(max_count, mx);
+    }
+    bs = (unsigned)__shfl((int)bs, 0);
+    bc = (unsigned)__shfl((int)bc, 0);
+    for (uint64_t b = s0; b < s1; b += 64) {
+        const uint64_t s = b + lane;
+        const uint64_t key = s < s1 ? t[s].key : kEmptyKey;
+        const bool occupied = key != kEmptyKey;
+        const uint32_t c = occupied ? t[s].count : 0;
+        const bool survive = occupied && c >= min_count;
+        const bool cand = occupied && (survive || keep_all);
+        const unsigned long long ms = __ballot(survive), mc = __ballot(cand);
+        if (survive) {
+            const unsigned id = bs + (unsigned)__popcll(ms & below);
+            t[s].dense = (int32_t)id;
+            if (skey) skey[id] = key;
+        }
+        if (cand) {
+            const unsigned k = bc + (unsigned)__popcll(mc & below);
+            cand_key[k] = key;
+            cand_count[k] = c;
+            cand_level[k] = (int8_t)level;
+        }
+        bs += (unsigned)__popcll(ms);
+        bc += (unsigned)__popcll(mc);
     }
 }
 
@@ -154,6 +196,27 @@ __global__ __launch_bounds__(kThreads) void k_count_at_least(const uint32_t* __r
     if ((threadIdx.x & 63) == 0 && m) atomicAdd(out, (unsigned long long)__popcll(m));
 }
 
+// Histogram of candidate counts, exact below kHistBins - 1 and pooled above:
+// a workgroup counts a run of candidates in LDS and adds its non-zero bins.
+constexpr int kHistBins = 4096;
+
+__global__ __launch_bounds__(kThreads) void k_count_hist(const uint32_t* __restrict__ cnt,
+                                                         int64_t n, int64_t per_block,
+                                                         unsigned long long* __restrict__ hist) {
+    __shared__ unsigned h[kHistBins];
+    for (int i = threadIdx.x; i < kHistBins; i += kThreads) h[i] = 0;
+    __syncthreads();
+    const int64_t i0 = (int64_t)blockIdx.x * per_block;
+    const int64_t i1 = i0 + per_block < n ? i0 + per_block : n;
+    for (int64_t i = i0 + threadIdx.x; i < i1; i += kThreads) {
+        const uint32_t c = cnt[i];
+        atomicAdd(&h[c < kHistBins - 1 ? c : kHistBins - 1], 1u);
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < kHistBins; i += kThreads)
+        if (h[i]) atomicAdd(hist + i, (unsigned long long)h[i]);
+}
+
 struct LevelKeys {
     const uint64_t* skey[SCONE_MAX_FGRAM_LEN + 1];  // survivors' codes by scan
 };
@@ -165,30 +228,55 @@ __global__ __launch_bounds__(kThreads) void k_select(
     int64_t S, LevelKeys lk, int max_len, unsigned* __restrict__ n_gt,
     unsigned* __restrict__ n_eq, int32_t* __restrict__ fgrams, int32_t* __restrict__ lengths,
     int32_t* __restrict__ counts) {
-    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (i >= n_cand) return;
-    const uint32_t c = cand_count[i];
-    int64_t pos = -1;
-    if (c > thresh) {
-        pos = atomicAdd(n_gt, 1u);
-    } else if (c == thresh) {
-        const int64_t e = atomicAdd(n_eq, 1u);
-        if (n_above + e < S) pos = n_above + e;
+    const int64_t i0 = ((int64_t)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6)) * kChunk;
+    if (i0 >= n_cand) return;  // wave-uniform
+    const int64_t i1 = i0 + kChunk < n_cand ? i0 + kChunk : n_cand;
+    const int lane = threadIdx.x & 63;
+    const unsigned long long below = (1ull << lane) - 1ull;
+    unsigned ng = 0, ne = 0;
+    for (int64_t b = i0; b < i1; b += 64) {
+        const int64_t i = b + lane;
+        const uint32_t c = i < i1 ? cand_count[i] : 0;
+        ng += (unsigned)__popcll(__ballot(i < i1 && c > thresh));
+        ne += (unsigned)__popcll(__ballot(i < i1 && c == thresh));
     }
-    if (pos < 0 || pos >= S) return;
-    const int level = cand_level[i];
-    int32_t tok[SCONE_MAX_FGRAM_LEN];
-    uint64_t key = cand_key[i];
-    for (int L = level; L >= 3; --L) {
-        tok[L - 1] = (int32_t)(key & 0xFFFF);
-        key = lk.skey[L - 1][key >> 16];
+    unsigned bg = 0, be = 0;
+    if (lane == 0) {
+        if (ng) bg = atomicAdd(n_gt, ng);
+        if (ne) be = atomicAdd(n_eq, ne);
     }
-    tok[1] = (int32_t)(key & 0xFFFF);
-    tok[0] = (int32_t)(key >> 16);
-    int32_t* row = fgrams + pos * (int64_t)max_len;
-    for (int j = 0; j < max_len; ++j) row[j] = j < level ? tok[j] : -1;
-    lengths[pos] = level;
-    counts[pos] = (int32_t)c;
+    bg = (unsigned)__shfl((int)bg, 0);
+    be = (unsigned)__shfl((int)be, 0);
+    for (int64_t b = i0; b < i1; b += 64) {
+        const int64_t i = b + lane;
+        const bool valid = i < i1;
+        const uint32_t c = valid ? cand_count[i] : 0;
+        const bool gt = valid && c > thresh, eq = valid && c == thresh;
+        const unsigned long long mg = __ballot(gt), me = __ballot(eq);
+        int64_t pos = -1;
+        if (gt) {
+            pos = bg + (unsigned)__popcll(mg & below);
+        } else if (eq) {
+            const int64_t e = be + (unsigned)__popcll(me & below);
+            if (n_above + e < S) pos = n_above + e;
+        }
+        bg += (unsigned)__popcll(mg);
+        be += (unsigned)__popcll(me);
+        if (pos < 0 || pos >= S) continue;
+        const int level = cand_level[i];
+        int32_t tok[SCONE_MAX_FGRAM_LEN];
+        uint64_t key = cand_key[i];
+        for (int L = level; L >= 3; --L) {
+            tok[L - 1] = (int32_t)(key & 0xFFFF);
+            key = lk.skey[L - 1][key >> 16];
+        }
+        tok[1] = (int32_t)(key & 0xFFFF);
+        tok[0] = (int32_t)(key >> 16);
+        int32_t* row = fgrams + pos * (int64_t)max_len;
+        for (int j = 0; j < max_len; ++j) row[j] = j < level ? tok[j] : -1;
+        lengths[pos] = level;
+        counts[pos] = (int32_t)c;
+    }
 }
 
 }  // namespace
@@ -238,6 +326,8 @@ extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_
     int8_t* cand_level = static_cast<int8_t*>(grab(cand_cap));
     unsigned* ctr = static_cast<unsigned*>(grab(16 * sizeof(unsigned)));
     unsigned long long* acc = static_cast<unsigned long long*>(grab(sizeof(unsigned long long)));
+    unsigned long long* hist =
+        static_cast<unsigned long long*>(grab(kHistBins * sizeof(unsigned long long)));
     LevelKeys lk{};
     uint64_t* skeys[SCONE_MAX_FGRAM_LEN + 1] = {};
     for (int L = 2; L < max_len; ++L) {
@@ -253,6 +343,11 @@ extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_
     int rc = SCONE_OK;
     const unsigned g_cap = (unsigned)((cap + kThreads - 1) / kThreads);
     const unsigned g_bt = (unsigned)((BT + kThreads - 1) / kThreads);
+    const int64_t waves_per_block = kThreads / 64;
+    auto chunk_grid = [&](int64_t n) {
+        const int64_t waves = (n + kChunk - 1) / kChunk;
+        return (unsigned)((waves + waves_per_block - 1) / waves_per_block);
+    };
     if (hipMemsetAsync(ctr, 0, 16 * sizeof(unsigned), st) != hipSuccess) rc = SCONE_EHIP;
     int32_t* ids_prev = ids_a;
     int32_t* ids_cur = ids_b;
@@ -261,7 +356,8 @@ extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_
         hipLaunchKernelGGL(k_count, dim3(g_bt), dim3(kThreads), 0, st, token_ids, BT, T, n,
                            ids_prev, table, mask, ctr + 0);
         if (hipMemsetAsync(ctr + 1, 0, sizeof(unsigned), st) != hipSuccess) rc = SCONE_EHIP;
-        hipLaunchKernelGGL(k_survivors, dim3(g_cap), dim3(kThreads), 0, st, table, cap,
+        hipLaunchKernelGGL(k_survivors, dim3(chunk_grid((int64_t)cap)), dim3(kThreads), 0, st,
+                           table, cap,
                            (uint32_t)min_count, n, n == 2 ? 1 : 0, ctr + 1,
                            n < max_len ? skeys[n] : nullptr, ctr + 2, cand_key, cand_count,
                            cand_level, ctr + 3);
@@ -297,20 +393,49 @@ extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_
     uint32_t thresh = 0;   // every candidate counts >= 1 > 0
     int64_t n_above = 0;   // candidates counting > thresh
     if (rc == SCONE_OK && n_cand > S) {
-        uint32_t lo = 1, hi = max_c;  // at_least(lo) = n_cand >= S
-        while (lo < hi && rc == SCONE_OK) {
-            const uint32_t mid = lo + (hi - lo + 1) / 2;
-            int64_t k = 0;
-            if (!at_least(mid, k)) rc = SCONE_EHIP;
-            else if (k >= S) lo = mid;
-            else hi = mid - 1;
+        // One pass: a histogram of the counts, exact below kHistBins - 1.
+        std::vector<unsigned long long> hh(kHistBins, 0);
+        const int64_t per_block = 65536;
+        if (hipMemsetAsync(hist, 0, kHistBins * sizeof(unsigned long long), st) != hipSuccess)
+            rc = SCONE_EHIP;
+        if (rc == SCONE_OK) {
+            hipLaunchKernelGGL(k_count_hist, dim3((unsigned)((n_cand + per_block - 1) / per_block)),
+                               dim3(kThreads), 0, st, cand_count, n_cand, per_block, hist);
+            if (hipGetLastError() != hipSuccess ||
+                hipMemcpyAsync(hh.data(), hist, kHistBins * sizeof(unsigned long long),
+                               hipMemcpyDeviceToHost, st) != hipSuccess ||
+                hipStreamSynchronize(st) != hipSuccess)
+                rc = SCONE_EHIP;
         }
-        thresh = lo;
-        if (rc == SCONE_OK && thresh < max_c && !at_least(thresh + 1, n_above)) rc = SCONE_EHIP;
+        if (rc == SCONE_OK && (int64_t)hh[kHistBins - 1] < S) {
+            // the threshold is below the pooled bin: read it off the histogram
+            int64_t ge = (int64_t)hh[kHistBins - 1];  // candidates counting >= c + 1
+            for (uint32_t c = kHistBins - 2; c >= 1; --c) {
+                const int64_t ge_c = ge + (int64_t)hh[c];
+                if (ge_c >= S) {
+                    thresh = c;
+                    n_above = ge;
+                    break;
+                }
+                ge = ge_c;
+            }
+        } else if (rc == SCONE_OK) {
+            // at least S candidates count >= kHistBins - 1: search the rest
+            uint32_t lo = kHistBins - 1, hi = max_c;  // at_least(lo) >= S
+            while (lo < hi && rc == SCONE_OK) {
+                const uint32_t mid = lo + (hi - lo + 1) / 2;
+                int64_t k = 0;
+                if (!at_least(mid, k)) rc = SCONE_EHIP;
+                else if (k >= S) lo = mid;
+                else hi = mid - 1;
+            }
+            thresh = lo;
+            if (rc == SCONE_OK && thresh < max_c && !at_least(thresh + 1, n_above))
+                rc = SCONE_EHIP;
+        }
     }
     if (rc == SCONE_OK && n_cand > 0) {
-        hipLaunchKernelGGL(k_select, dim3((unsigned)((n_cand + kThreads - 1) / kThreads)),
-                           dim3(kThreads), 0, st, cand_key, cand_count, cand_level, n_cand, thresh,
+        hipLaunchKernelGGL(k_select, dim3(chunk_grid(n_cand)), dim3(kThreads), 0, st, cand_key, cand_count, cand_level, n_cand, thresh,
                            n_above, S, lk, max_len, ctr + 4, ctr + 5, fgrams, lengths, counts);
         if (hipGetLastError() != hipSuccess) rc = SCONE_EHIP;
     }

@@ -13,7 +13,7 @@ import oracle
 from oracle import discovery
 import paper_2502_01637_amd as S
 from gpu_util import build_gpu, dev
-from workloads import CONFIGS, make_workload, scaled, query_batches
+from workloads import CONFIGS, make_workload, scaled, query_batches, zipf_cdf, zipf_tokens
 
 pytestmark = pytest.mark.gpu
 
@@ -78,6 +78,19 @@ def test_discovery_zipf_corpus_and_round_trip():
     S.check_ok()
     np.testing.assert_array_equal(got_ids.cpu().numpy(), exp_ids)
     np.testing.assert_array_equal(got_len.cpu().numpy(), exp_len)
+
+
+def test_discovery_threshold_above_the_histogram():
+    """A small S over a corpus whose top n-grams count in the tens of
+    thousands: the count threshold lies above the exact range of the device
+    histogram, so the search over the pooled counts decides it."""
+    rng = np.random.default_rng(31)
+    X = zipf_tokens(rng, zipf_cdf(40), (16, 125_000)).astype(np.int32)
+    for K, Sn, mc in [(3, 3, 5), (2, 10, 1), (3, 40, 5)]:
+        cands = discovery.candidates(X, K, mc)
+        assert cands[Sn - 1][1] >= 4096
+        fg, ln, ct = S.discover_fgrams(dev(X), K, Sn, mc)
+        check_top_s(fg, ln, ct, cands, Sn)
 
 
 def test_discovery_edges_and_errors():
