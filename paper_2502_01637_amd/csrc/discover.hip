@@ -68,36 +68,81 @@ __device__ __forceinline__ uint64_t ngram_code(const int32_t* __restrict__ X,
     return ((uint64_t)p << 16) | tok;
 }
 
-__global__ __launch_bounds__(kThreads) void k_count(const int32_t* __restrict__ X, int64_t BT,
-                                                    int64_t T, int n,
-                                                    const int32_t* __restrict__ ids_prev,
-                                                    CountSlot* __restrict__ t, uint64_t mask,
-                                                    unsigned* __restrict__ status) {
-    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (i >= BT) return;
-    if (n == 2) {
-        const int32_t tok = X[i];
-        if (tok < 0 || tok >= SCONE_TOKEN_LIMIT) {
-            atomicOr(status, err_bit(SCONE_ETOKEN));
-            return;
-        }
-    }
-    const int64_t tt = i % T;
-    const uint64_t key = ngram_code(X, ids_prev, i, tt, n);
-    if (key == kEmptyKey) return;
-    if (n == 2 && (X[i - 1] < 0 || X[i - 1] >= SCONE_TOKEN_LIMIT)) return;  // reported there
+// Add c to key's count in the global table; false if the table is full.
+__device__ __forceinline__ bool global_add(CountSlot* __restrict__ t, uint64_t mask,
+                                           uint64_t key, uint32_t c) {
     uint64_t s = count_hash(key) & mask;
     for (uint64_t step = 0; step <= mask; ++step) {
         const unsigned long long old = atomicCAS(reinterpret_cast<unsigned long long*>(&t[s].key),
                                                  (unsigned long long)kEmptyKey,
                                                  (unsigned long long)key);
         if (old == kEmptyKey || old == key) {
-            atomicAdd(&t[s].count, 1u);
-            return;
+            atomicAdd(&t[s].count, c);
+            return true;
         }
         s = (s + 1) & mask;
     }
-    atomicOr(status, err_bit(SCONE_EFULL));
+    return false;
+}
+
+// Counting is aggregated per workgroup first: a workgroup counts
+// kCountPerBlock consecutive positions in an LDS table, then adds each
+// distinct key to the global table once.  Frequent n-grams (a Zipf stream's
+// top bigram is about 1% of all positions) would otherwise serialise hundreds
+// of thousands of increments on one global slot.  Keys that find no LDS slot
+// within kLdsProbe probes go straight to the global table.
+constexpr int kCountPerBlock = 4096;
+constexpr int kLdsSlots = 4096;
+constexpr int kLdsProbe = 32;
+
+__global__ __launch_bounds__(kThreads) void k_count(const int32_t* __restrict__ X, int64_t BT,
+                                                    int64_t T, int n,
+                                                    const int32_t* __restrict__ ids_prev,
+                                                    CountSlot* __restrict__ t, uint64_t mask,
+                                                    unsigned* __restrict__ status) {
+    __shared__ unsigned long long s_key[kLdsSlots];
+    __shared__ unsigned s_cnt[kLdsSlots];
+    for (int j = threadIdx.x; j < kLdsSlots; j += kThreads) {
+        s_key[j] = (unsigned long long)kEmptyKey;
+        s_cnt[j] = 0;
+    }
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kCountPerBlock;
+    bool full = false, bad_token = false;
+    for (int r = 0; r < kCountPerBlock / kThreads; ++r) {
+        const int64_t i = base + r * kThreads + threadIdx.x;
+        if (i >= BT) break;
+        if (n == 2) {
+            const int32_t tok = X[i];
+            if (tok < 0 || tok >= SCONE_TOKEN_LIMIT) {
+                bad_token = true;
+                continue;
+            }
+        }
+        const uint64_t key = ngram_code(X, ids_prev, i, i % T, n);
+        if (key == kEmptyKey) continue;
+        if (n == 2 && (X[i - 1] < 0 || X[i - 1] >= SCONE_TOKEN_LIMIT)) continue;  // reported there
+        uint32_t h = (uint32_t)count_hash(key) & (kLdsSlots - 1);
+        bool done = false;
+        for (int q = 0; q < kLdsProbe; ++q) {
+            const unsigned long long old =
+                atomicCAS(&s_key[h], (unsigned long long)kEmptyKey, (unsigned long long)key);
+            if (old == kEmptyKey || old == key) {
+                atomicAdd(&s_cnt[h], 1u);
+                done = true;
+                break;
+            }
+            h = (h + 1) & (kLdsSlots - 1);
+        }
+        if (!done && !global_add(t, mask, key, 1u)) full = true;
+    }
+    __syncthreads();
+    for (int j = threadIdx.x; j < kLdsSlots; j += kThreads) {
+        const unsigned long long key = s_key[j];
+        if (key != kEmptyKey && !global_add(t, mask, key, s_cnt[j])) full = true;
+    }
+    if (bad_token) atomicOr(status, err_bit(SCONE_ETOKEN));
+    if (full) atomicOr(status, err_bit(SCONE_EFULL));
 }
 
 // Dense ids for the survivors (count >= min_count) and, for scan 2, every
@@ -353,7 +398,8 @@ extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_
     int32_t* ids_cur = ids_b;
     for (int n = 2; n <= max_len && rc == SCONE_OK; ++n) {
         hipLaunchKernelGGL(k_table_clear, dim3(g_cap), dim3(kThreads), 0, st, table, cap);
-        hipLaunchKernelGGL(k_count, dim3(g_bt), dim3(kThreads), 0, st, token_ids, BT, T, n,
+        hipLaunchKernelGGL(k_count, dim3((unsigned)((BT + kCountPerBlock - 1) / kCountPerBlock)),
+                           dim3(kThreads), 0, st, token_ids, BT, T, n,
                            ids_prev, table, mask, ctr + 0);
         if (hipMemsetAsync(ctr + 1, 0, sizeof(unsigned), st) != hipSuccess) rc = SCONE_EHIP;
         hipLaunchKernelGGL(k_survivors, dim3(chunk_grid((int64_t)cap)), dim3(kThreads), 0, st,
