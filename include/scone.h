@@ -118,8 +118,8 @@ int scone_lookup(const scone_table_t* table, const int32_t* token_ids, int64_t B
 /*
  * Pre-scan tagging (the paper tags every training token with the length of
  * its longest matching f-gram before training, implementation details in the
- * appendix; the mean of these lengths is the "average match length" of
- * Section 4.1): the match lengths of scone_lookup without the ids, plus
+ * appendix; the mean of these lengths is the average match length that
+ * Section 4.1 reports): the match lengths of scone_lookup without the ids, plus
  * their histogram.
  *
  *  token_ids  [B, T] int32, as for scone_lookup.
