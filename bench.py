@@ -1,12 +1,16 @@
 #!/usr/bin/env python3
 """Benchmark of the f-gram embedding hot path on one MI355X.
 
-One step is one pass of the whole path over one [B, T] batch already resident
-on the device: the longest-suffix lookup (scone_lookup) followed by the row
-gather (scone_gather).  The table build is offline and not timed.  Prints one
-JSON line with tokens/s, the gather's achieved bandwidth against its roofline
-(HBM, or PCIe when the rows live in host-pinned memory), and the CPU oracle
-timed on a bounded sample of the same workload.
+One step is one pass of the whole path over one [B, T] batch's worth of work,
+inputs already resident on the device: the longest-suffix lookup and the row
+gather.  The headline schedule is the library's pipelined step
+(scone_embed_pipelined): each launch gathers the rows of batch k while it
+looks up batch k+1, so K timed steps run K lookups and K gathers.  The serial
+schedule (scone_lookup then scone_gather) and the fused kernel (scone_embed)
+are timed beside it.  The table build is offline and not timed.  Prints one
+JSON line with tokens/s, the step kernel's achieved bandwidth against its
+roofline (HBM, or PCIe when the rows live in host-pinned memory), and the CPU
+oracle timed on a bounded sample of the same workload.
 
 Workloads (``--config``): c2_1m (default), c3_10m_k5, tiny (HBM prefill),
 c4_host (rows in host-pinned memory read over PCIe), c5_decode (256
@@ -53,14 +57,25 @@ def describe(cfg) -> str:
             f"max_n={cfg.max_n}")
 
 
-def source_sha(name: str) -> str:
-    p = os.path.join(ROOT, "paper_2502_01637_amd", "csrc", name)
-    return hashlib.sha1(open(p, "rb").read()).hexdigest()[:12]
+# The sources of each measured kernel (its file and the headers that hold its
+# device code): a traffic summary is used only while they are unchanged.
+KERNEL_SOURCES = {
+    "gather": ("gather.hip", "row_copy.h"),
+    "embed": ("embed.hip", "tile_lookup.h"),
+    "pipelined": ("pipeline.hip", "row_copy.h", "tile_lookup.h"),
+}
 
 
-def measured_traffic(config: str, kernel: str, kernel_src: str):
+def source_sha(*names: str) -> str:
+    h = hashlib.sha1()
+    for name in names:
+        h.update(open(os.path.join(ROOT, "paper_2502_01637_amd", "csrc", name), "rb").read())
+    return h.hexdigest()[:12]
+
+
+def measured_traffic(config: str, kernel: str):
     """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
-    summary, or None when there is none for this kernel source."""
+    summary, or None when there is none for the kernel's current sources."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{config}_traffic.md")
     if not os.path.exists(path):
         return None
@@ -68,7 +83,7 @@ def measured_traffic(config: str, kernel: str, kernel_src: str):
     if not m:
         return None
     rec = json.loads(m.group(1))
-    if rec.get("source_sha1") != source_sha(kernel_src):
+    if rec.get("source_sha1") != source_sha(*KERNEL_SOURCES[kernel]):
         return None
     return rec
 
@@ -209,6 +224,7 @@ def cpu_baseline(cfg, w, X0, host_np_full, E, gpu_ids, gpu_outs, min_seconds: fl
              "seconds": round(elapsed, 3), "build_seconds": round(build_s, 3)},
             {"ids_bit_exact": bool(np.array_equal(gpu_ids, exp_ids)),
              "split_rows_bit_exact": parity_rows[0], "fused_rows_bit_exact": parity_rows[1],
+             "pipelined_rows_bit_exact": parity_rows[2],
              "positions": int(cfg.n_tok)}, exp_len)
 
 
@@ -233,6 +249,9 @@ def run_prefill(args, cfg):
         rows = E
     X = [torch.from_numpy(b).to(dev) for b in batches_np]
     fid = torch.empty((cfg.B, cfg.T), dtype=torch.int32, device=dev)
+    # the pipelined schedule's two id buffers: step g gathers pid[g % 2] (batch
+    # g's ids, looked up by step g - 1) and looks up batch g + 1 into the other
+    pid = [torch.empty((cfg.B, cfg.T), dtype=torch.int32, device=dev) for _ in range(2)]
     # Step k writes outs[k % N_BATCHES]: together the outputs exceed the 256 MB
     # last-level cache, so no step overwrites lines the previous one left
     # dirty there and every step's writes reach HBM.
@@ -245,15 +264,23 @@ def run_prefill(args, cfg):
 
     K = args.steps
 
+    def pipelined_step(g):
+        S.embed_pipelined(table, X[(g + 1) % N_BATCHES], cfg.max_n, pid[(g + 1) % 2],
+                          pid[g % 2], rows, out=outs[g % N_BATCHES])
+
     def timed(path):
         """W warm-up steps, then K timed steps between two synchronisations.
         HIP events around each kernel are recorded on every 8th step only, so
         that they barely perturb the wall clock.  Returns (wall seconds,
         per-kernel mean ms list)."""
+        if path == "pipelined":   # first lookup, before the warm-up steps
+            S.embed_pipelined(table, X[0], cfg.max_n, pid[0], None, rows)
         for k in range(args.warmup):
             if path == "split":
                 S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
                 S.gather(fid, rows, out=outs[k % N_BATCHES])
+            elif path == "pipelined":
+                pipelined_step(k)
             else:
                 S.embed(table, X[k % N_BATCHES], cfg.max_n, rows, out=outs[k % N_BATCHES])
         rc = S.check()
@@ -261,8 +288,10 @@ def run_prefill(args, cfg):
             raise SystemExit(f"device error after warmup ({path}): status {rc}")
         nk = 2 if path == "split" else 1
         ev = []
+        span = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         torch.cuda.synchronize()
         t0 = time.perf_counter()
+        span[0].record()
         for k in range(K):
             e = None
             if k % SAMPLE_EVERY == 0:
@@ -274,25 +303,38 @@ def run_prefill(args, cfg):
                 if e:
                     e[1].record()
                 S.gather(fid, rows, out=outs[k % N_BATCHES])
+            elif path == "pipelined":
+                pipelined_step(args.warmup + k)
             else:
                 S.embed(table, X[k % N_BATCHES], cfg.max_n, rows, out=outs[k % N_BATCHES])
             if e:
                 e[nk].record()
+        span[1].record()
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
         rc = S.check()
         if rc != 0:
             raise SystemExit(f"device error in timed region ({path}): status {rc}")
         per = [float(np.mean([e[i].elapsed_time(e[i + 1]) for e in ev])) for i in range(nk)]
-        return wall, per
+        return wall, per, span[0].elapsed_time(span[1]) / K
 
-    # The headline path is the library's two calls, scone_lookup then
-    # scone_gather; the fused scone_embed is timed the same way beside it.
-    wall, (lookup_ms, gather_ms) = timed("split")
-    fused_wall, (embed_ms,) = timed("fused")
+    # The headline is the pipelined schedule (one launch per step); the serial
+    # schedule, scone_lookup then scone_gather, and the fused scone_embed are
+    # timed the same way beside it.
+    # The pipelined path launches one kernel per step, so its launch duration
+    # is the device time of the whole timed region (two events around it) per
+    # step; the events around single sampled launches (also reported) read a
+    # few microseconds high, as each adds its own marker packets.
+    wall, (pipe_sampled_ms,), pipe_ms = timed("pipelined")
+    serial_wall, (lookup_ms, gather_ms), _ = timed("split")
+    fused_wall, (embed_ms,), _ = timed("fused")
 
     gather_bytes = cfg.gather_bytes()
     achieved = gather_bytes / (gather_ms * 1e-3) / 1e9
+    # one pipelined launch: the gather's bytes plus the lookup's token read
+    # and id write (hash probes are the lookup's cost, not the problem's)
+    pipe_bytes = gather_bytes + cfg.n_tok * 8
+    pipe_achieved = pipe_bytes / (pipe_ms * 1e-3) / 1e9
     embed_bytes = cfg.n_tok * (4 + 2 * cfg.row_bytes)
     embed_achieved = embed_bytes / (embed_ms * 1e-3) / 1e9
     value = cfg.n_tok * K / wall
@@ -320,7 +362,7 @@ def run_prefill(args, cfg):
     cold = None
     if not host:
         flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
-        ce = []
+        ce, pe = [], []
         for k in range(COLD_REPS):
             flush.amax()
             e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
@@ -330,14 +372,26 @@ def run_prefill(args, cfg):
             S.gather(fid, rows, out=outs[k % N_BATCHES])
             e[2].record()
             ce.append(e)
+        S.embed_pipelined(table, X[0], cfg.max_n, pid[0], None, rows)
+        for k in range(COLD_REPS):
+            flush.amax()
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            e[0].record()
+            pipelined_step(k)
+            e[1].record()
+            pe.append(e)
         torch.cuda.synchronize()
         del flush
         c_look = float(np.mean([e[0].elapsed_time(e[1]) for e in ce]))
         c_gath = float(np.mean([e[1].elapsed_time(e[2]) for e in ce]))
+        c_pipe = float(np.mean([e[0].elapsed_time(e[1]) for e in pe]))
         cold = {"reps": COLD_REPS, "flush_bytes": 1 << 30, "lookup_us": c_look * 1e3,
                 "gather_us": c_gath * 1e3,
                 "gather_GBps": gather_bytes / (c_gath * 1e-3) / 1e9,
-                "device_tokens_per_s": cfg.n_tok / ((c_look + c_gath) * 1e-3)}
+                "device_tokens_per_s": cfg.n_tok / ((c_look + c_gath) * 1e-3),
+                "pipelined_us": c_pipe * 1e3,
+                "pipelined_GBps": pipe_bytes / (c_pipe * 1e-3) / 1e9,
+                "pipelined_device_tokens_per_s": cfg.n_tok / (c_pipe * 1e-3)}
 
     if args.copy_calibration:
         n = args.copy_calibration << 20
@@ -352,6 +406,8 @@ def run_prefill(args, cfg):
     fid0, ml0 = S.lookup(table, X[0], cfg.max_n, want_len=True)
     out0 = S.gather(fid0, rows)
     out0f = S.embed(table, X[0], cfg.max_n, rows)
+    S.embed_pipelined(table, X[0], cfg.max_n, pid[0], None, rows)
+    out0p = S.embed_pipelined(table, X[1], cfg.max_n, pid[1], pid[0], rows)
     if S.check() != 0:
         raise SystemExit("device error in parity pass")
     torch.cuda.synchronize()
@@ -361,7 +417,7 @@ def run_prefill(args, cfg):
     if host:
         # rows cross PCIe once; the output is written to HBM
         read_bytes = cfg.n_tok * cfg.row_bytes
-        pcie = read_bytes / (gather_ms * 1e-3) / 1e9
+        pcie = read_bytes / (pipe_ms * 1e-3) / 1e9
         ceiling = h2d_ceiling(torch, dev)
         bound, peak, rate = "pcie", PCIE_PEAK_GBPS, pcie
         extra = {"pcie_read_GBps": pcie, "h2d_copy_ceiling_GBps": ceiling,
@@ -369,9 +425,9 @@ def run_prefill(args, cfg):
                  "pcie_inclusive_tokens_per_s": value, "split_placement": split}
         alg_bytes = read_bytes
     else:
-        bound, peak, rate = "hbm", HBM_PEAK_GBPS, achieved
+        bound, peak, rate = "hbm", HBM_PEAK_GBPS, pipe_achieved
         extra = {}
-        alg_bytes = gather_bytes
+        alg_bytes = pipe_bytes
 
     result = {
         "metric": METRIC,
@@ -391,7 +447,13 @@ def run_prefill(args, cfg):
                    "row_bytes": cfg.row_bytes, "placement": cfg.placement,
                    "hash_slots": table.capacity, "slot_bytes": table.slot_bytes,
                    "rotating_batches": N_BATCHES},
-        "path": "scone_lookup + scone_gather",
+        "path": "scone_embed_pipelined (one launch per step: gather of batch k, lookup of "
+                "batch k+1)",
+        "pipelined_us": pipe_ms * 1e3,
+        "pipelined_us_sampled_single_launch": pipe_sampled_ms * 1e3,
+        "serial_path": {"path": "scone_lookup + scone_gather",
+                        "tokens_per_s": cfg.n_tok * K / serial_wall,
+                        "ms_per_step": serial_wall * 1e3 / K},
         "lookup_us": lookup_ms * 1e3,
         "gather_us": gather_ms * 1e3,
         "gather_GBps": achieved,
@@ -408,14 +470,17 @@ def run_prefill(args, cfg):
                               / HBM_PEAK_GBPS},
     }
     result.update(extra)
-    traffic = measured_traffic(cfg.name, "gather", "gather.hip")
+    traffic = measured_traffic(cfg.name, "pipelined")
     result["roofline"] = {
         "bound": bound, "achieved": rate, "peak": peak, "unit": "GB/s", "frac": rate / peak,
         "traffic": None if traffic is None else traffic["traffic_bytes_per_launch"],
-        "kernel": "scone_gather (k_gather_rows)",
+        "kernel": "scone_embed_pipelined (k_pipelined)",
         "algorithmic_bytes_per_launch": alg_bytes,
     }
-    etraffic = measured_traffic(cfg.name, "embed", "embed.hip")
+    gtraffic = measured_traffic(cfg.name, "gather")
+    result["serial_path"]["gather_traffic"] = (None if gtraffic is None
+                                               else gtraffic["traffic_bytes_per_launch"])
+    etraffic = measured_traffic(cfg.name, "embed")
     result["fused_path"]["traffic"] = (None if etraffic is None
                                        else etraffic["traffic_bytes_per_launch"])
     ml = ml0.cpu().numpy()
@@ -425,7 +490,8 @@ def run_prefill(args, cfg):
     if not args.no_cpu_baseline:
         host_np = rows.tensor().view(torch.uint8).numpy() if host else None
         cb, parity, exp_len = cpu_baseline(cfg, w, batches_np[0], host_np, E,
-                                           fid0.cpu().numpy(), [out0, out0f], args.cpu_seconds)
+                                           fid0.cpu().numpy(), [out0, out0f, out0p],
+                                           args.cpu_seconds)
         parity["match_len_bit_exact"] = bool(np.array_equal(ml, exp_len))
         result["cpu_baseline"] = cb
         result["parity"] = parity

@@ -172,6 +172,38 @@ int scone_embed(const scone_table_t* table, const int32_t* token_ids, int64_t B,
                 void* stream);
 
 /*
+ * One step of a stream of batches, software-pipelined (Algorithm 1's
+ * inference branch, the lookup of one batch overlapped with the gather of
+ * the batch before it): in a single launch,
+ *   next_ids[b, t] = scone_lookup's id for next_tokens[b, t]   (next batch)
+ *   out[k, :]      = rows[cur_ids[k], :]                        (current batch)
+ * The results equal scone_lookup on the next batch and scone_gather on the
+ * current ids.  A stream of batches X_0, X_1, ... runs as: step 0 with no
+ * current ids (lookup of X_0 only), step k with next = X_k and cur = the ids
+ * of X_{k-1}, and a last step with no next tokens (gather only); the ids
+ * alternate between two buffers.
+ *
+ *  next_tokens, B, T, max_n   as for scone_lookup; B * T == 0 (next_tokens
+ *             may then be NULL) makes this step a gather only.
+ *  next_ids   [B, T] int32 output; next_len [B, T] int8 output or NULL.
+ *  cur_ids    [n_cur] int32, the previous step's next_ids; n_cur == 0
+ *             (cur_ids may then be NULL) makes this step a lookup only.
+ *  rows, n_rows, row_bytes, placement   as for scone_gather.
+ *  out        [n_cur, row_bytes] device output.
+ *
+ * Returns SCONE_EINVAL when next_ids or next_len share memory with cur_ids
+ * (the launch writes one while it reads the other); otherwise errors as for
+ * scone_lookup and scone_gather.  Rows of 1, 2, 4 or 8 KiB, 16-byte aligned,
+ * take the one-launch kernel; other widths run the lookup and gather kernels
+ * back to back with the same results.  Asynchronous on `stream`.
+ */
+int scone_embed_pipelined(const scone_table_t* table, const int32_t* next_tokens, int64_t B,
+                          int64_t T, int32_t max_n, int32_t* next_ids, int8_t* next_len,
+                          const int32_t* cur_ids, int64_t n_cur, const void* rows,
+                          int64_t n_rows, int64_t row_bytes, int32_t placement, void* out,
+                          void* stream);
+
+/*
  * One decoding step for S sequences (inference emits one token per step per
  * sequence; Section 4.3 measures per-token latency this way).  Sequence s
  * appends new_tok[s] to its rolling context and gets the embedding of the

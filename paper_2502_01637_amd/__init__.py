@@ -7,10 +7,11 @@ Python binding.
 """
 from . import scone
 from .scone import (SconeError, Table, HostRows, build_fgram_table, lookup, gather, embed,
+                    embed_pipelined,
                     decode_step, gather_split, split_workspace_bytes, tag, discover_fgrams,
                     FgramModel, precompute_fgram_rows, check, check_ok)
 
 __all__ = ["scone", "SconeError", "Table", "HostRows", "build_fgram_table", "lookup", "gather",
-           "embed", "decode_step", "gather_split", "split_workspace_bytes", "tag", "discover_fgrams",
+           "embed", "embed_pipelined", "decode_step", "gather_split", "split_workspace_bytes", "tag", "discover_fgrams",
            "FgramModel", "precompute_fgram_rows", "check",
            "check_ok"]

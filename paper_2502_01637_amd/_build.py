@@ -7,7 +7,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libscone.so")
 SOURCES = ["runtime.hip", "table_build.hip", "lookup.hip", "gather.hip", "embed.hip", "decode.hip",
-           "gather_split.hip", "discover.hip", "fgram_model.hip"]
+           "gather_split.hip", "discover.hip", "fgram_model.hip", "pipeline.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

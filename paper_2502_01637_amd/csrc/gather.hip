@@ -12,7 +12,7 @@
 // the caches leaves them to the table rows that repeat (frequent tokens).
 // The same kernel reads a host-mapped pinned table over PCIe when the rows
 // live off the accelerator.
-#include "scone_internal.h"
+#include "row_copy.h"
 
 namespace scone {
 namespace {
@@ -73,8 +73,7 @@ __global__ __launch_bounds__(kGatherThreads) void k_gather(
 }
 
 // Rows of 64*U 16-byte units (1, 2, 4 or 8 KiB): one wavefront per row, four
-// rows per workgroup.  The row id is wave-uniform, so it is read once into a
-// scalar register and every load is a scalar row base plus the lane offset.
+// rows per workgroup.
 template <int U>
 __global__ __launch_bounds__(kGatherThreads) void k_gather_rows(
     const int32_t* __restrict__ ids, int64_t n_tok, const u32x4* __restrict__ rows,
@@ -82,17 +81,7 @@ __global__ __launch_bounds__(kGatherThreads) void k_gather_rows(
     const int64_t r = (int64_t)blockIdx.x * (kGatherThreads / 64) +
                       __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (r >= n_tok) return;  // wave-uniform
-    const int lane = threadIdx.x & 63;
-    const int64_t id = ids[r];
-    const bool ok = (id >= 0) & (id < n_rows);
-    const u32x4* src = rows + (ok ? id : 0) * (64 * U);
-    u32x4 v[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) v[u] = src[u * 64 + lane];
-    u32x4* dst = out + r * (64 * U);
-#pragma unroll
-    for (int u = 0; u < U; ++u) __builtin_nontemporal_store(ok ? v[u] : u32x4{}, dst + u * 64 + lane);
-    if (!ok && lane == 0) atomicOr(err, err_bit(SCONE_EROW));
+    copy_row_wave<U>(ids, r, rows, n_rows, out, err);
 }
 
 // Every id is out of range when the table has no rows: zero the output.
@@ -142,6 +131,36 @@ hipError_t launch_zero_rows(void* out, int64_t bytes, unsigned* err, hipStream_t
     return hipGetLastError();
 }
 
+hipError_t launch_gather_any(const int32_t* ids, int64_t n_tok, const void* rows, int64_t n_rows,
+                             int64_t row_bytes, void* out, unsigned* err, hipStream_t st) {
+    // Widest unit that divides the row width and both base addresses.
+    const uintptr_t align = (uintptr_t)rows | (uintptr_t)out | (uintptr_t)row_bytes;
+    const int64_t upr16 = row_bytes / 16;
+    if ((align & 15) == 0 && n_rows > 0 &&
+        (upr16 == 64 || upr16 == 128 || upr16 == 256 || upr16 == 512)) {
+        const int64_t grid = (n_tok + kGatherThreads / 64 - 1) / (kGatherThreads / 64);
+        if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+        const u32x4* R = static_cast<const u32x4*>(rows);
+        u32x4* O = static_cast<u32x4*>(out);
+        switch (upr16) {
+            case 64: hipLaunchKernelGGL(k_gather_rows<1>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, ids, n_tok, R, n_rows, O, err); break;
+            case 128: hipLaunchKernelGGL(k_gather_rows<2>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, ids, n_tok, R, n_rows, O, err); break;
+            case 256: hipLaunchKernelGGL(k_gather_rows<4>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, ids, n_tok, R, n_rows, O, err); break;
+            default: hipLaunchKernelGGL(k_gather_rows<8>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, ids, n_tok, R, n_rows, O, err); break;
+        }
+        return hipGetLastError();
+    }
+    if ((align & 15) == 0)
+        return launch_gather<u32x4, 4>(ids, n_tok, rows, n_rows, row_bytes, out, err, st);
+    if ((align & 7) == 0)
+        return launch_gather<u32x2, 4>(ids, n_tok, rows, n_rows, row_bytes, out, err, st);
+    if ((align & 3) == 0)
+        return launch_gather<uint32_t, 4>(ids, n_tok, rows, n_rows, row_bytes, out, err, st);
+    if ((align & 1) == 0)
+        return launch_gather<uint16_t, 4>(ids, n_tok, rows, n_rows, row_bytes, out, err, st);
+    return launch_gather<uint8_t, 4>(ids, n_tok, rows, n_rows, row_bytes, out, err, st);
+}
+
 }  // namespace scone
 
 extern "C" int scone_gather(const int32_t* fgram_ids, int64_t n_tok, const void* rows,
@@ -155,34 +174,8 @@ extern "C" int scone_gather(const int32_t* fgram_ids, int64_t n_tok, const void*
     if (!fgram_ids || !out || (!rows && n_rows > 0)) return SCONE_EINVAL;
     unsigned* err = device_error_word();
     if (!err) return SCONE_EHIP;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    // Widest unit that divides the row width and both base addresses.
-    const uintptr_t align = (uintptr_t)rows | (uintptr_t)out | (uintptr_t)row_bytes;
-    hipError_t e;
-    const int64_t upr16 = row_bytes / 16;
-    if ((align & 15) == 0 && n_rows > 0 &&
-        (upr16 == 64 || upr16 == 128 || upr16 == 256 || upr16 == 512)) {
-        const int64_t grid = (n_tok + kGatherThreads / 64 - 1) / (kGatherThreads / 64);
-        if (grid > 0x7fffffffLL) return SCONE_EINVAL;
-        const u32x4* R = static_cast<const u32x4*>(rows);
-        u32x4* O = static_cast<u32x4*>(out);
-        switch (upr16) {
-            case 64: hipLaunchKernelGGL(k_gather_rows<1>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, fgram_ids, n_tok, R, n_rows, O, err); break;
-            case 128: hipLaunchKernelGGL(k_gather_rows<2>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, fgram_ids, n_tok, R, n_rows, O, err); break;
-            case 256: hipLaunchKernelGGL(k_gather_rows<4>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, fgram_ids, n_tok, R, n_rows, O, err); break;
-            default: hipLaunchKernelGGL(k_gather_rows<8>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, fgram_ids, n_tok, R, n_rows, O, err); break;
-        }
-        e = hipGetLastError();
-    } else if ((align & 15) == 0)
-        e = launch_gather<u32x4, 4>(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err, st);
-    else if ((align & 7) == 0)
-        e = launch_gather<u32x2, 4>(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err, st);
-    else if ((align & 3) == 0)
-        e = launch_gather<uint32_t, 4>(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err, st);
-    else if ((align & 1) == 0)
-        e = launch_gather<uint16_t, 4>(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err, st);
-    else
-        e = launch_gather<uint8_t, 4>(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err, st);
+    const hipError_t e = launch_gather_any(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err,
+                                           static_cast<hipStream_t>(stream));
     if (e == hipErrorInvalidConfiguration) return SCONE_EINVAL;
     return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
 }

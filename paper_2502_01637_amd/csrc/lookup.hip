@@ -24,21 +24,9 @@ __global__ __launch_bounds__(kTileThreads) void k_lookup(
     __shared__ int32_t s_tok[P + kMaxHalo];
     __shared__ unsigned s_hist[SCONE_MAX_FGRAM_LEN + 1];
     if (hist && threadIdx.x <= SCONE_MAX_FGRAM_LEN) s_hist[threadIdx.x] = 0;
-    const int64_t b = blockIdx.x / tiles_per_row;
-    const int64_t t0 = (blockIdx.x - b * tiles_per_row) * (int64_t)P;
-    stage_tokens(s_tok, X + b * T, T, t0, P, max_n - 1);
-    __syncthreads();
-    int32_t id;
-    int len;
-    bool tok_ok;
-    tile_lookup<SB, G>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok);
-    const int64_t t = t0 + threadIdx.x / G;
-    if (threadIdx.x % G == 0 && t < T) {
-        if (!tok_ok) atomicOr(err, err_bit(SCONE_ETOKEN));
-        if (ids_out) ids_out[b * T + t] = id;
-        if (len_out) len_out[b * T + t] = (int8_t)len;
-        if (hist) atomicAdd(&s_hist[len], 1u);
-    }
+    const int len = lookup_block<SB, G>(slots, mask, X, T, max_n, tiles_per_row, blockIdx.x,
+                                        s_tok, ids_out, len_out, err);
+    if (hist && len) atomicAdd(&s_hist[len], 1u);
     if (hist) {  // uniform: the whole workgroup takes this branch or none does
         __syncthreads();
         if (threadIdx.x <= SCONE_MAX_FGRAM_LEN && s_hist[threadIdx.x])

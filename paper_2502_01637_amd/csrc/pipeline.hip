@@ -1,0 +1,147 @@
+// Pipelined inference step: the lookup of batch k+1 and the row gather of
+// batch k in one launch (Algorithm 1's inference branch, software-pipelined
+// across batches).
+//
+// The lookup is latency-bound (dependent hash probes, a few KiB per tile) and
+// the gather is HBM-bound (streaming rows).  Run back to back, the lookup
+// launch leaves the memory system idle while its probes wait and the gather
+// launch pays its ramp-up and tail on its own.  Here the first workgroups of
+// the grid run tile lookups of the next batch and the rest copy rows of the
+// current one, so the probes of the lookup workgroups overlap the row stream
+// of the gather workgroups on every compute unit.  The ids of step k were
+// written by step k-1, so the two halves share no data within a launch.
+// Lookup workgroups come first in the grid: they are dispatched before the
+// gather workgroups and their long probe chains start early.
+#include "row_copy.h"
+#include "tile_lookup.h"
+
+namespace scone {
+namespace {
+
+template <int SB, int G, int U>
+__global__ __launch_bounds__(kTileThreads) void k_pipelined(
+    const typename SlotOps<SB>::Slot* __restrict__ slots, uint64_t mask,
+    const int32_t* __restrict__ X, int64_t T, int max_n, int64_t tiles_per_row,
+    int64_t n_lookup_blocks, int32_t* __restrict__ next_ids, int8_t* __restrict__ next_len,
+    const int32_t* __restrict__ cur_ids, int64_t n_cur, const u32x4* __restrict__ rows,
+    int64_t n_rows, u32x4* __restrict__ out, unsigned* __restrict__ err) {
+    __shared__ int32_t s_tok[TileShape<G>::kPositions + kMaxHalo];
+    if ((int64_t)blockIdx.x < n_lookup_blocks) {  // workgroup-uniform
+        lookup_block<SB, G>(slots, mask, X, T, max_n, tiles_per_row, blockIdx.x, s_tok,
+                            next_ids, next_len, err);
+        return;
+    }
+    const int64_t r = ((int64_t)blockIdx.x - n_lookup_blocks) * (kTileThreads / 64) +
+                      __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (r >= n_cur) return;  // wave-uniform
+    copy_row_wave<U>(cur_ids, r, rows, n_rows, out, err);
+}
+
+struct Step {
+    const scone_table* tb;
+    const int32_t* X;
+    int64_t B, T;
+    int max_n;
+    int32_t* next_ids;
+    int8_t* next_len;
+    const int32_t* cur_ids;
+    int64_t n_cur;
+    const void* rows;
+    int64_t n_rows;
+    void* out;
+    unsigned* err;
+    hipStream_t st;
+};
+
+template <int SB, int G, int U>
+hipError_t launch(const Step& s) {
+    using Slot = typename SlotOps<SB>::Slot;
+    constexpr int P = TileShape<G>::kPositions;
+    const int64_t tiles = (s.T + P - 1) / P;
+    const int64_t n_lookup = s.B * tiles;
+    const int64_t n_gather = (s.n_cur + kTileThreads / 64 - 1) / (kTileThreads / 64);
+    if (n_lookup + n_gather > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((k_pipelined<SB, G, U>), dim3((unsigned)(n_lookup + n_gather)),
+                       dim3(kTileThreads), 0, s.st, static_cast<const Slot*>(s.tb->slots),
+                       (uint64_t)s.tb->capacity - 1, s.X, s.T, s.max_n, tiles, n_lookup,
+                       s.next_ids, s.next_len, s.cur_ids, s.n_cur,
+                       static_cast<const u32x4*>(s.rows), s.n_rows, static_cast<u32x4*>(s.out),
+                       s.err);
+    return hipGetLastError();
+}
+
+template <int SB, int G>
+hipError_t by_units(const Step& s, int units) {
+    switch (units) {
+        case 1: return launch<SB, G, 1>(s);
+        case 2: return launch<SB, G, 2>(s);
+        case 4: return launch<SB, G, 4>(s);
+        default: return launch<SB, G, 8>(s);
+    }
+}
+
+template <int SB>
+hipError_t by_lanes(const Step& s, int units) {
+    switch (lanes_for(s.max_n)) {
+        case 1: return by_units<SB, 1>(s, units);
+        case 2: return by_units<SB, 2>(s, units);
+        case 4: return by_units<SB, 4>(s, units);
+        default: return by_units<SB, 8>(s, units);
+    }
+}
+
+bool overlaps(const void* a, int64_t a_bytes, const void* b, int64_t b_bytes) {
+    if (!a || !b || a_bytes == 0 || b_bytes == 0) return false;
+    const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
+    return pa < pb + (uintptr_t)b_bytes && pb < pa + (uintptr_t)a_bytes;
+}
+
+}  // namespace
+}  // namespace scone
+
+extern "C" int scone_embed_pipelined(const scone_table_t* table, const int32_t* next_tokens,
+                                     int64_t B, int64_t T, int32_t max_n, int32_t* next_ids,
+                                     int8_t* next_len, const int32_t* cur_ids, int64_t n_cur,
+                                     const void* rows, int64_t n_rows, int64_t row_bytes,
+                                     int32_t placement, void* out, void* stream) {
+    using namespace scone;
+    if (!table || B < 0 || T < 0 || max_n < 1 || n_cur < 0 || n_rows < 0 || row_bytes <= 0)
+        return SCONE_EINVAL;
+    if (placement != SCONE_PLACE_HBM && placement != SCONE_PLACE_HOST) return SCONE_EINVAL;
+    if (B > 0 && T > ((int64_t)1 << 62) / B) return SCONE_EINVAL;
+    if (n_cur > ((int64_t)1 << 62) / row_bytes) return SCONE_EINVAL;
+    const int64_t n_next = B * T;
+    if (n_next > 0 && (!next_tokens || !next_ids)) return SCONE_EINVAL;
+    if (n_cur > 0 && (!cur_ids || !out || (!rows && n_rows > 0))) return SCONE_EINVAL;
+    // The lookup writes while the gather reads: the next batch's outputs must
+    // not share memory with the current batch's ids.
+    if (n_next > 0 && n_cur > 0 &&
+        (overlaps(next_ids, n_next * 4, cur_ids, n_cur * 4) ||
+         overlaps(next_len, n_next, cur_ids, n_cur * 4)))
+        return SCONE_EINVAL;
+    int dev = 0;
+    SCONE_HIP_TRY(hipGetDevice(&dev));
+    if (dev != table->device) return SCONE_EINVAL;
+    if (n_next == 0 && n_cur == 0) return SCONE_OK;
+    unsigned* err = device_error_word();
+    if (!err) return SCONE_EHIP;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int eff = max_n < table->max_len ? max_n : table->max_len;
+    const int units = wave_row_units(row_bytes);
+    const bool aligned = (((uintptr_t)rows | (uintptr_t)out) & 15) == 0;
+    hipError_t e = hipSuccess;
+    if (n_next > 0 && n_cur > 0 && units > 0 && aligned && n_rows > 0) {
+        const Step s{table, next_tokens, B, T, eff, next_ids, next_len, cur_ids, n_cur,
+                     rows, n_rows, out, err, st};
+        e = table->slot_bytes == 16 ? by_lanes<16>(s, units) : by_lanes<32>(s, units);
+    } else {
+        // One half empty, or rows the one-wavefront copy does not cover: the
+        // two kernels of scone_lookup and scone_gather, back to back.
+        if (n_next > 0)
+            e = launch_lookup(table, next_tokens, B, T, eff, next_ids, next_len, err, st);
+        if (e == hipSuccess && n_cur > 0)
+            e = launch_gather_any(cur_ids, n_cur, rows, n_rows, row_bytes, out, err, st);
+    }
+    if (e == hipErrorInvalidConfiguration) return SCONE_EINVAL;
+    return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
+}

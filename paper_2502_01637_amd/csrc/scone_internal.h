@@ -188,6 +188,10 @@ hipError_t launch_lookup(const scone_table* tb, const int32_t* X, int64_t B, int
 // Zero `bytes` of device memory with a kernel and raise SCONE_EROW (a table
 // without rows has no valid row id).
 hipError_t launch_zero_rows(void* out, int64_t bytes, unsigned* err, hipStream_t st);
+// Launch the gather kernel that suits the row width and alignment (the whole of
+// scone_gather after its argument checks).
+hipError_t launch_gather_any(const int32_t* ids, int64_t n_tok, const void* rows, int64_t n_rows,
+                             int64_t row_bytes, void* out, unsigned* err, hipStream_t st);
 }  // namespace scone
 
 // The opaque table handle.

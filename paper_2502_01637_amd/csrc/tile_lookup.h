@@ -68,4 +68,37 @@ __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __
     len_out = gm ? max_n - jb : 1;
 }
 
+// One workgroup's share of a lookup over X [B, T]: tile `tile` of the row-major
+// tile grid (tiles_per_row tiles of P positions per row).  Stages the tile's
+// tokens in s_tok, finds each position's longest match and writes the id and
+// length (either output may be null); a bad token raises SCONE_ETOKEN.
+// Returns the matched length on the lane that wrote a position, else 0.
+// Called by the whole workgroup (it synchronises once).
+template <int SB, int G>
+__device__ __forceinline__ int lookup_block(const typename SlotOps<SB>::Slot* __restrict__ slots,
+                                            uint64_t mask, const int32_t* __restrict__ X,
+                                            int64_t T, int max_n, int64_t tiles_per_row,
+                                            int64_t tile, int32_t* s_tok,
+                                            int32_t* __restrict__ ids_out,
+                                            int8_t* __restrict__ len_out,
+                                            unsigned* __restrict__ err) {
+    constexpr int P = TileShape<G>::kPositions;
+    const int64_t b = tile / tiles_per_row;
+    const int64_t t0 = (tile - b * tiles_per_row) * (int64_t)P;
+    stage_tokens(s_tok, X + b * T, T, t0, P, max_n - 1);
+    __syncthreads();
+    int32_t id;
+    int len;
+    bool tok_ok;
+    tile_lookup<SB, G>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok);
+    const int64_t t = t0 + threadIdx.x / G;
+    if (threadIdx.x % G == 0 && t < T) {
+        if (!tok_ok) atomicOr(err, err_bit(SCONE_ETOKEN));
+        if (ids_out) ids_out[b * T + t] = id;
+        if (len_out) len_out[b * T + t] = (int8_t)len;
+        return len;
+    }
+    return 0;
+}
+
 }  // namespace scone

@@ -45,6 +45,9 @@ def _declare(L):
     L.scone_gather.restype = I
     L.scone_embed.argtypes = [P, P, I64, I64, I32, P, I64, I64, I32, P, P, P, P]
     L.scone_embed.restype = I
+    L.scone_embed_pipelined.argtypes = [P, P, I64, I64, I32, P, P, P, I64, P, I64, I64, I32, P,
+                                        P]
+    L.scone_embed_pipelined.restype = I
     L.scone_decode_step.argtypes = [P, P, P, I32, P, I64, I32, P, I64, I64, I32, P, P, P, P]
     L.scone_decode_step.restype = I
     L.scone_discover_fgrams.argtypes = [P, I64, I64, I32, I32, I64, P, P, P,
@@ -410,6 +413,46 @@ def embed(table: Table, token_ids: torch.Tensor, max_n: int, rows, out=None,
                                row_bytes, placement, _ptr(out), _ptr(fgram_ids), _ptr(match_len),
                                _stream(stream))
     _check(rc, "scone_embed")
+    return out
+
+
+def embed_pipelined(table: Table, next_tokens: Optional[torch.Tensor], max_n: int,
+                    next_ids: Optional[torch.Tensor], cur_ids: Optional[torch.Tensor], rows,
+                    out: Optional[torch.Tensor] = None, next_len: Optional[torch.Tensor] = None,
+                    stream=None) -> Optional[torch.Tensor]:
+    """scone_embed_pipelined: in one launch, look up next_tokens [B, T] into
+    next_ids and gather the rows of cur_ids into out [*cur_ids.shape, *row_shape].
+    Either half may be None (lookup only, or gather only).  Returns out."""
+    placement, base, n_rows, row_bytes, row_shape, dtype = _rows_arg(rows)
+    B = T = 0
+    if next_tokens is not None:
+        _dev_i32(next_tokens, "next_tokens", 2)
+        B, T = next_tokens.shape
+        if next_ids is None:
+            raise ValueError("next_ids is required with next_tokens")
+        _dev_i32(next_ids, "next_ids")
+        if next_ids.numel() != B * T:
+            raise ValueError("next_ids has the wrong size")
+        if next_len is not None and (next_len.dtype != torch.int8 or next_len.numel() != B * T
+                                     or not next_len.is_contiguous()):
+            raise ValueError("next_len must be a contiguous int8 tensor of B*T elements")
+    n_cur = 0
+    if cur_ids is not None:
+        _dev_i32(cur_ids, "cur_ids")
+        n_cur = cur_ids.numel()
+        if out is None:
+            out = torch.empty(tuple(cur_ids.shape) + row_shape, dtype=dtype,
+                              device=cur_ids.device)
+        if not out.is_contiguous() or out.numel() * out.element_size() != n_cur * row_bytes:
+            raise ValueError("out must be contiguous with n_cur * row_bytes bytes")
+    device = next_tokens.device if next_tokens is not None else (
+        cur_ids.device if cur_ids is not None else table.device)
+    with torch.cuda.device(device):
+        rc = lib().scone_embed_pipelined(
+            table.handle, _ptr(next_tokens), B, T, int(max_n), _ptr(next_ids), _ptr(next_len),
+            _ptr(cur_ids), n_cur, base, n_rows, row_bytes, placement, _ptr(out),
+            _stream(stream))
+    _check(rc, "scone_embed_pipelined")
     return out
 
 

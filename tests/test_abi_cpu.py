@@ -56,6 +56,9 @@ def test_host_side_argument_errors():
     assert L.scone_gather(None, 1, None, 1, 16, None, 7, None) == E
     assert L.scone_gather(None, 1, None, 1, 16, None, 0, None) == E
     assert L.scone_gather(None, 0, None, 0, 16, None, 0, None) == S.scone.OK  # nothing to do
+    # pipelined step: no table, bad window, negative sizes, bad placement
+    assert L.scone_embed_pipelined(None, None, 0, 0, 3, None, None, None, 0, None, 0, 16, 0,
+                                   None, None) == E
     # host memory and table bookkeeping
     assert L.scone_host_alloc(0, ctypes.byref(h), ctypes.byref(h)) == E
     assert L.scone_host_free(None) == S.scone.OK

@@ -57,8 +57,11 @@ def test_hbm_prefill_full_size(name):
     o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
     tb = build_gpu(w.fgrams, w.lengths, w.ids, max_load=0.5)
     E = device_rows(cfg)
-    for k, X in enumerate(query_batches(w, 2)):
+    batches = query_batches(w, 2)
+    expected = []
+    for k, X in enumerate(batches):
         exp_ids, exp_len = o.lookup(X, cfg.max_n)
+        expected.append(exp_ids)
         ids, ml = S.lookup(tb, dev(X), cfg.max_n, want_len=True)
         out = S.gather(ids, E)
         S.check_ok()
@@ -70,6 +73,18 @@ def test_hbm_prefill_full_size(name):
         S.check_ok()
         assert torch.equal(fused.view(torch.int16), out.view(torch.int16)), (name, k)
         del out, fused
+    # the pipelined schedule bench.py times: lookup of batch k+1 and gather of
+    # batch k in one launch, ids alternating between two buffers
+    Xd = [dev(X) for X in batches]
+    ids_buf = [torch.empty(X.shape, dtype=torch.int32, device="cuda") for X in batches]
+    S.embed_pipelined(tb, Xd[0], cfg.max_n, ids_buf[0], None, E)
+    outs = [S.embed_pipelined(tb, Xd[1], cfg.max_n, ids_buf[1], ids_buf[0], E),
+            S.embed_pipelined(tb, None, cfg.max_n, None, ids_buf[1], E)]
+    S.check_ok()
+    for k, out in enumerate(outs):
+        np.testing.assert_array_equal(ids_buf[k].cpu().numpy(), expected[k])
+        assert rows_match_generator(cfg, out, expected[k]), (name, "pipelined", k)
+        assert sampled_oracle_rows(cfg, out, expected[k], seed=10 + k), (name, "pipelined", k)
 
 
 def test_host_pinned_full_size():
