@@ -339,21 +339,33 @@ def run_prefill(args, cfg):
     embed_achieved = embed_bytes / (embed_ms * 1e-3) / 1e9
     value = cfg.n_tok * K / wall
 
-    # Uniform-random-id control at the same shape: no Zipf reuse to help the caches.
+    # Two controls at the same shape, each rotating N_BATCHES distinct id sets
+    # like the query batches (one set reused every step would leave its rows
+    # in the 256 MB last-level cache): uniform random ids (no Zipf reuse to
+    # help the caches) and contiguous rows (the kernel's streaming rate with
+    # neither reuse nor random access).
     gen = torch.Generator(device=dev)
     gen.manual_seed(cfg.seed)
-    uid = torch.randint(0, cfg.n_rows, (cfg.B, cfg.T), dtype=torch.int32, device=dev,
-                        generator=gen)
-    for k in range(2):
-        S.gather(uid, rows, out=outs[k % N_BATCHES])
-    torch.cuda.synchronize()
-    ue = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    ue[0].record()
-    for k in range(K):
-        S.gather(uid, rows, out=outs[k % N_BATCHES])
-    ue[1].record()
-    torch.cuda.synchronize()
-    uniform_ms = ue[0].elapsed_time(ue[1]) / K
+    uids = [torch.randint(0, cfg.n_rows, (cfg.B, cfg.T), dtype=torch.int32, device=dev,
+                          generator=gen) for _ in range(N_BATCHES)]
+    sids = [(torch.arange(k * cfg.n_tok, (k + 1) * cfg.n_tok, dtype=torch.int64, device=dev)
+             % cfg.n_rows).to(torch.int32).view(cfg.B, cfg.T) for k in range(N_BATCHES)]
+
+    def control_ms(idsets):
+        for k in range(2):
+            S.gather(idsets[k % N_BATCHES], rows, out=outs[k % N_BATCHES])
+        torch.cuda.synchronize()
+        ue = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ue[0].record()
+        for k in range(K):
+            S.gather(idsets[k % N_BATCHES], rows, out=outs[k % N_BATCHES])
+        ue[1].record()
+        torch.cuda.synchronize()
+        return ue[0].elapsed_time(ue[1]) / K
+
+    uniform_ms = control_ms(uids)
+    sequential_ms = control_ms(sids)
+    del uids, sids
 
     # Cold caches: reading a 1 GiB buffer between repetitions evicts the L2s
     # and the 256 MB last-level cache, so table, hash slots and tokens all come
@@ -467,7 +479,11 @@ def run_prefill(args, cfg):
         "uniform_id_gather": {"us": uniform_ms * 1e3,
                               "GBps": gather_bytes / (uniform_ms * 1e-3) / 1e9,
                               "pct_hbm_peak": 100.0 * gather_bytes / (uniform_ms * 1e-3) / 1e9
-                              / HBM_PEAK_GBPS},
+                              / HBM_PEAK_GBPS, "id_sets": N_BATCHES},
+        "sequential_row_gather": {"us": sequential_ms * 1e3,
+                                  "GBps": gather_bytes / (sequential_ms * 1e-3) / 1e9,
+                                  "pct_hbm_peak": 100.0 * gather_bytes / (sequential_ms * 1e-3)
+                                  / 1e9 / HBM_PEAK_GBPS, "id_sets": N_BATCHES},
     }
     result.update(extra)
     traffic = measured_traffic(cfg.name, "pipelined")
