@@ -3,7 +3,7 @@
 //
 //   C[m, n] = sum_k A[m, k] * W[n, k] + bias[n]        (A [M, K], W [N, K])
 //   kBias:  out_bf16[m, n]  = bf16(C)
-//   kGelu:  out_bf16[m, n]  = bf16(GELU(C))             (exact, erf form)
+//   kGelu:  out_bf16[m, n]  = bf16(GELU(C))             (erf form)
 //   kResid: out_f32[m, n]  += C                         (the residual stream)
 //
 // Both operands are K-contiguous.  A workgroup computes a BM x BN tile over
@@ -11,7 +11,11 @@
 // memory straight into LDS (global_load_lds_dwordx4: no registers, no LDS
 // write instructions); the next slab is in flight while the current one is
 // multiplied, and the only synchronisation per slab is a counted wait on the
-// wavefront's own copies plus a workgroup barrier.  Each wavefront owns a
+// wavefront's own copies plus a workgroup barrier.  Fragments are double
+// buffered in registers: a slab is two 32-deep halves, and the LDS reads of
+// one half are in flight while the matrix cores multiply the other, so the
+// products of a slab's second half run after the barrier while the next
+// slab's first fragments load.  Each wavefront owns a
 // (BM / WGM) x (BN / WGN) part of the tile as 16 x 16 v_mfma_f32_16x16x32_bf16
 // tiles.  W is the instruction's first operand and A the second, so a lane's
 // four accumulators are four consecutive n of one row m: the epilogue writes
@@ -45,8 +49,24 @@ __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
     return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
+// GELU(x) = x Phi(x) = x (1 + erf(x / sqrt 2)) / 2, with erf from
+// Abramowitz and Stegun 7.1.26 (Hastings' rational approximation):
+// erf(z) = 1 - t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) exp(-z^2),
+// t = 1 / (1 + p z), z >= 0, absolute error at most 1.5e-7, odd in z.  The
+// outputs are rounded to bf16 (relative step 2^-8), so the approximation is
+// invisible in them; it costs one reciprocal and one exp2 on the hardware
+// units instead of a full-precision erf.
 __device__ __forceinline__ float gelu_erf(float x) {
-    return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f));
+    const float z = fabsf(x) * 0.70710678118654752f;
+    const float t = __builtin_amdgcn_rcpf(1.0f + 0.3275911f * z);
+    float q = 1.061405429f;
+    q = q * t - 1.453152027f;
+    q = q * t + 1.421413741f;
+    q = q * t - 0.284496736f;
+    q = q * t + 0.254829592f;
+    const float e = __builtin_amdgcn_exp2f(-(z * z) * 1.4426950408889634f);  // exp(-z^2)
+    const float erf_abs = 1.0f - q * t * e;
+    return 0.5f * x * (1.0f + (x < 0.0f ? -erf_abs : erf_abs));
 }
 
 // s_waitcnt immediates (gfx9 encoding): wait until at most n vector-memory
@@ -120,49 +140,66 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
 #pragma unroll
         for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    const int KT = K / kBK;
-    issue(0, 0);
     const int fr = lane & 15;                          // fragment row
     const int swz = lane & 7;                          // fragment row & 7
     const int q0 = lane >> 4;                          // fragment k chunk
-    for (int kt = 0; kt < KT; ++kt) {
-        // Slab kt is this wavefront's only outstanding copy; after the
-        // barrier every wavefront's part of it is in LDS, and every
-        // wavefront has finished reading the other stage.
-        __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
-        __builtin_amdgcn_s_barrier();
-        if (kt + 1 < KT) issue(kt + 1, (kt + 1) & 1);
-        const uint8_t* sA = smem + (kt & 1) * STAGE;
+    // Fragments of 32-deep half `ks` of the slab in `stage`.
+    auto read = [&](int stage, int ks, bf16x8* fw, bf16x8* fa) {
+        const uint8_t* sA = smem + stage * STAGE;
         const uint8_t* sW = sA + BM * kRowBytes;
+        const int slot = ((ks * 4 + q0) ^ swz) * 16;
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            const int slot = ((ks * 4 + q0) ^ swz) * 16;
-            bf16x8 fw[TN], fa[TM];
+        for (int i = 0; i < TN; ++i)
+            fw[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
+                sW + (wn * WTN + i * 16 + fr) * kRowBytes + slot));
 #pragma unroll
-            for (int i = 0; i < TN; ++i)
-                fw[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                    sW + (wn * WTN + i * 16 + fr) * kRowBytes + slot));
+        for (int j = 0; j < TM; ++j)
+            fa[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
+                sA + (wm * WTM + j * 16 + fr) * kRowBytes + slot));
+    };
+    auto multiply = [&](const bf16x8* fw, const bf16x8* fa) {
+#pragma unroll
+        for (int i = 0; i < TN; ++i)
 #pragma unroll
             for (int j = 0; j < TM; ++j)
-                fa[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                    sA + (wm * WTM + j * 16 + fr) * kRowBytes + slot));
-#pragma unroll
-            for (int i = 0; i < TN; ++i)
-#pragma unroll
-                for (int j = 0; j < TM; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[i], fa[j], acc[i][j],
-                                                                        0, 0, 0);
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fw[i], fa[j], acc[i][j],
+                                                                    0, 0, 0);
+    };
+
+    const int KT = K / kBK;
+    bf16x8 f0w[TN], f0a[TM], f1w[TN], f1a[TM];  // halves 0 and 1 of a slab
+    issue(0, 0);
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    if (KT > 1) issue(1, 1);
+    read(0, 0, f0w, f0a);
+    for (int kt = 0; kt < KT; ++kt) {
+        read(kt & 1, 1, f1w, f1a);
+        multiply(f0w, f0a);
+        __builtin_amdgcn_sched_barrier(0);
+        if (kt + 1 < KT) {
+            // Half 1 of slab kt has landed, so this wavefront reads nothing
+            // more from stage kt & 1, and its copies of slab kt + 1 are in
+            // LDS; after the barrier the same holds for every wavefront:
+            // slab kt + 1 is readable and stage kt & 1 may be refilled.
+            __builtin_amdgcn_s_waitcnt(kWaitLds);
+            __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+            if (kt + 2 < KT) issue(kt + 2, kt & 1);
+            read((kt + 1) & 1, 0, f0w, f0a);
         }
-        // this stage's reads are done before any wavefront passes the next
-        // barrier and refills it
-        __builtin_amdgcn_s_waitcnt(kWaitLds);
+        multiply(f1w, f1a);
+        __builtin_amdgcn_sched_barrier(0);
     }
 
     // acc[i][j][r] = C[m, n] with n = n0 + wn*WTN + i*16 + (lane/16)*4 + r and
     // m = m0 + wm*WTM + j*16 + lane%16.  Every load the epilogue needs (the
-    // biases, and for kResid a column group's residual values) is issued
-    // before its first use, so a wavefront waits once per group instead of
-    // once per 16 x 16 tile; rows past M read row M - 1 and are not stored.
+    // biases, and for kResid the residual values of up to four column groups)
+    // is issued before its first use, so a wavefront waits once per round
+    // instead of once per 16 x 16 tile; rows past M read row M - 1 and are
+    // not stored.
     u32x2 bb[TN];
 #pragma unroll
     for (int i = 0; i < TN; ++i)
@@ -173,22 +210,35 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
         const float b0 = bf16_to_f32(bb[i].x & 0xFFFFu), b1 = bf16_to_f32(bb[i].x >> 16);
         const float b2 = bf16_to_f32(bb[i].y & 0xFFFFu), b3 = bf16_to_f32(bb[i].y >> 16);
         if (EPI == kResid) {
+            // G column groups per round: their G * TM residual loads are all
+            // in flight before the first add.
+            constexpr int G = TN < 4 ? TN : 4;
+            if (i % G != 0) continue;
             float* o = static_cast<float*>(out);
-            f32x4 h[TM];
+            f32x4 h[G][TM];
 #pragma unroll
-            for (int j = 0; j < TM; ++j) {
-                const int m = m0 + wm * WTM + j * 16 + (lane & 15);
-                h[j] = *reinterpret_cast<const f32x4*>(o + (int64_t)(m < M ? m : M - 1) * ldc + n);
-            }
+            for (int g = 0; g < G; ++g)
 #pragma unroll
-            for (int j = 0; j < TM; ++j) {
-                const int m = m0 + wm * WTM + j * 16 + (lane & 15);
-                if (m >= M) continue;
-                h[j][0] += acc[i][j][0] + b0;
-                h[j][1] += acc[i][j][1] + b1;
-                h[j][2] += acc[i][j][2] + b2;
-                h[j][3] += acc[i][j][3] + b3;
-                *reinterpret_cast<f32x4*>(o + (int64_t)m * ldc + n) = h[j];
+                for (int j = 0; j < TM; ++j) {
+                    const int m = m0 + wm * WTM + j * 16 + (lane & 15);
+                    h[g][j] = *reinterpret_cast<const f32x4*>(
+                        o + (int64_t)(m < M ? m : M - 1) * ldc + n + g * 16);
+                }
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const u32x2 bg = bb[i + g];
+                const float c0 = bf16_to_f32(bg.x & 0xFFFFu), c1 = bf16_to_f32(bg.x >> 16);
+                const float c2 = bf16_to_f32(bg.y & 0xFFFFu), c3 = bf16_to_f32(bg.y >> 16);
+#pragma unroll
+                for (int j = 0; j < TM; ++j) {
+                    const int m = m0 + wm * WTM + j * 16 + (lane & 15);
+                    if (m >= M) continue;
+                    h[g][j][0] += acc[i + g][j][0] + c0;
+                    h[g][j][1] += acc[i + g][j][1] + c1;
+                    h[g][j][2] += acc[i + g][j][2] + c2;
+                    h[g][j][3] += acc[i + g][j][3] + c3;
+                    *reinterpret_cast<f32x4*>(o + (int64_t)m * ldc + n + g * 16) = h[g][j];
+                }
             }
         } else {
 #pragma unroll
@@ -224,12 +274,14 @@ inline hipError_t launch_tiles(const uint16_t* A, const uint16_t* W, const uint1
 // elements (ldc >= N, a multiple of 4).  Large products take 256 x 256 tiles
 // on eight wavefronts (half the LDS and L2 traffic per flop of 128 x 128);
 // N not a multiple of 256, or too few tiles to fill the 256 compute units,
-// take 128 x 128 on four.
+// take 128 x 128 on four.  The eight wavefronts of a 256 x 256 tile own
+// 64 x 128 parts (four down, two across): measured faster than 128 x 64
+// parts on every product of the f-gram model.
 template <int EPI>
 inline hipError_t launch(const uint16_t* A, const uint16_t* W, const uint16_t* bias, void* out,
                          int64_t ldc, int M, int N, int K, hipStream_t st) {
     if (N % 256 == 0 && (int64_t)((M + 255) / 256) * (N / 256) >= 256)
-        return launch_tiles<EPI, 256, 256, 2, 4>(A, W, bias, out, ldc, M, N, K, st);
+        return launch_tiles<EPI, 256, 256, 4, 2>(A, W, bias, out, ldc, M, N, K, st);
     return launch_tiles<EPI, 128, 128, 2, 2>(A, W, bias, out, ldc, M, N, K, st);
 }
 
