@@ -364,10 +364,12 @@ int scone_host_alloc(int64_t bytes, void** host_ptr, void** device_ptr);
 int scone_host_free(void* host_ptr);
 
 /*
- * Wait for `stream`, then read and clear the current device's error word.
- * Returns SCONE_OK or the lowest data-error code raised by the asynchronous
- * calls since the last check (SCONE_ETOKEN, SCONE_EROW, SCONE_EFULL).  The
- * word is per device, not per stream: concurrent streams share it.
+ * Wait for `stream`, then read the current device's error word and clear
+ * the bits it read (atomically, so a bit that a kernel on another stream
+ * raises after the read is kept for the next check).  Returns SCONE_OK or
+ * the lowest data-error code raised by the asynchronous calls since the last
+ * check (SCONE_ETOKEN, SCONE_EROW, SCONE_EFULL).  The word is per device, not
+ * per stream: concurrent streams share it.
  */
 int scone_check(void* stream);
 

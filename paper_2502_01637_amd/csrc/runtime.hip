@@ -33,6 +33,12 @@ unsigned* device_error_word() {
     return g_err_word[dev];
 }
 
+namespace {
+// Clears exactly the bits the host read, so that a bit another stream's
+// kernel raised after the read survives until the next check.
+__global__ void k_clear_bits(unsigned* word, unsigned bits) { atomicAnd(word, ~bits); }
+}  // namespace
+
 }  // namespace scone
 
 extern "C" {
@@ -43,8 +49,13 @@ int scone_check(void* stream) {
     unsigned* w = scone::device_error_word();
     if (!w) return SCONE_EHIP;
     unsigned h = 0;
-    SCONE_HIP_TRY(hipMemcpy(&h, w, sizeof(h), hipMemcpyDeviceToHost));
-    if (h) SCONE_HIP_TRY(hipMemset(w, 0, sizeof(unsigned)));
+    SCONE_HIP_TRY(hipMemcpyAsync(&h, w, sizeof(h), hipMemcpyDeviceToHost, st));
+    SCONE_HIP_TRY(hipStreamSynchronize(st));
+    if (h) {
+        hipLaunchKernelGGL(scone::k_clear_bits, dim3(1), dim3(1), 0, st, w, h);
+        SCONE_HIP_TRY(hipGetLastError());
+        SCONE_HIP_TRY(hipStreamSynchronize(st));
+    }
     return scone::code_from_bits(h);
 }
 
