@@ -498,6 +498,13 @@ def run_prefill(args, cfg):
     etraffic = measured_traffic(cfg.name, "embed")
     result["fused_path"]["traffic"] = (None if etraffic is None
                                        else etraffic["traffic_bytes_per_launch"])
+    # Space of the f-gram layer as served: the row table plus the dictionary
+    # (the paper's in-memory layout, a dense matrix and a hash index).
+    result["space"] = {"row_table_bytes": cfg.n_rows * cfg.row_bytes,
+                       "hash_table_bytes": table.capacity * table.slot_bytes,
+                       "total_bytes": cfg.n_rows * cfg.row_bytes
+                       + table.capacity * table.slot_bytes,
+                       "hash_load": table.n / table.capacity}
     ml = ml0.cpu().numpy()
     result["match"] = match_stats(ml, cfg.max_n)
     result["build_ms"] = build_s * 1e3
