@@ -21,8 +21,9 @@ __global__ __launch_bounds__(kDecodeThreads) void k_decode(
     const typename SlotOps<SB>::Slot* __restrict__ slots, uint64_t mask, int32_t* __restrict__ ctx,
     int32_t* __restrict__ ctx_len, int ctx_cap, const int32_t* __restrict__ new_tok, int max_n,
     const V* __restrict__ rows, int64_t n_rows, int64_t upr, int shift, V* __restrict__ out,
-    int32_t* __restrict__ ids_out, int8_t* __restrict__ len_out, unsigned* __restrict__ err) {
-    const int64_t s = blockIdx.x;
+    int32_t* __restrict__ ids_out, int8_t* __restrict__ len_out, unsigned* __restrict__ err,
+    int64_t block0) {
+    const int64_t s = block_index(block0);
     const int lane = threadIdx.x;
     int32_t* my_ctx = ctx + s * ctx_cap;
     // The length, the new token and the whole context are loaded at once (the
@@ -102,11 +103,12 @@ hipError_t launch(const scone_table* tb, int32_t* ctx, int32_t* ctx_len, int ctx
                   int64_t n_rows, int64_t upr, int shift, void* out, int32_t* ids, int8_t* lens,
                   unsigned* err, hipStream_t st) {
     using Slot = typename SlotOps<SB>::Slot;
-    hipLaunchKernelGGL((k_decode<SB, G, V, 4, kPow2>), dim3((unsigned)S), dim3(kDecodeThreads),
-                       0, st, static_cast<const Slot*>(tb->slots), (uint64_t)tb->capacity - 1,
-                       ctx, ctx_len, ctx_cap, new_tok, max_n, static_cast<const V*>(rows), n_rows,
-                       upr, shift, static_cast<V*>(out), ids, lens, err);
-    return hipGetLastError();
+    return launch_blocks(S, kDecodeThreads, [&](int64_t b0, dim3 grid) {
+        hipLaunchKernelGGL((k_decode<SB, G, V, 4, kPow2>), grid, dim3(kDecodeThreads), 0, st,
+                           static_cast<const Slot*>(tb->slots), (uint64_t)tb->capacity - 1, ctx,
+                           ctx_len, ctx_cap, new_tok, max_n, static_cast<const V*>(rows), n_rows,
+                           upr, shift, static_cast<V*>(out), ids, lens, err, b0);
+    });
 }
 
 template <int SB, typename V, bool kPow2>
@@ -155,7 +157,7 @@ extern "C" int scone_decode_step(const scone_table_t* table, int32_t* ctx, int32
     if (placement != SCONE_PLACE_HBM && placement != SCONE_PLACE_HOST) return SCONE_EINVAL;
     const int eff = max_n < table->max_len ? max_n : table->max_len;
     if (ctx_cap < eff - 1 || ctx_cap > 63 || ctx_cap < 0) return SCONE_EINVAL;
-    if (S > 0x7fffffffLL || S > ((int64_t)1 << 62) / row_bytes) return SCONE_EINVAL;
+    if (S > ((int64_t)1 << 62) / row_bytes) return SCONE_EINVAL;
     if (S == 0) return SCONE_OK;
     if (!ctx_len || !new_tok || !out || (!ctx && ctx_cap > 0) || (!rows && n_rows > 0))
         return SCONE_EINVAL;

@@ -45,8 +45,8 @@ __device__ __forceinline__ uint64_t count_hash(uint64_t key) {
 constexpr int kChunk = 4096;
 
 __global__ __launch_bounds__(kThreads) void k_table_clear(CountSlot* __restrict__ t,
-                                                          uint64_t cap) {
-    const uint64_t i = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
+                                                          uint64_t cap, int64_t block0) {
+    const uint64_t i = (uint64_t)block_index(block0) * kThreads + threadIdx.x;
     if (i < cap) {
         t[i].key = kEmptyKey;
         t[i].count = 0;
@@ -212,8 +212,9 @@ __global__ __launch_bounds__(kThreads) void k_ids(const int32_t* __restrict__ X,
                                                   int64_t T, int n,
                                                   const int32_t* __restrict__ ids_prev,
                                                   const CountSlot* __restrict__ t, uint64_t mask,
-                                                  int32_t* __restrict__ ids_cur) {
-    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+                                                  int32_t* __restrict__ ids_cur,
+                                                  int64_t block0) {
+    const int64_t i = block_index(block0) * kThreads + threadIdx.x;
     if (i >= BT) return;
     const uint64_t key = ngram_code(X, ids_prev, i, i % T, n);
     int32_t d = -1;
@@ -234,8 +235,9 @@ __global__ __launch_bounds__(kThreads) void k_ids(const int32_t* __restrict__ X,
 
 __global__ __launch_bounds__(kThreads) void k_count_at_least(const uint32_t* __restrict__ cnt,
                                                              int64_t n, uint32_t c,
-                                                             unsigned long long* __restrict__ out) {
-    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+                                                             unsigned long long* __restrict__ out,
+                                                             int64_t block0) {
+    const int64_t i = block_index(block0) * kThreads + threadIdx.x;
     const bool hit = i < n && cnt[i] >= c;
     const unsigned long long m = __ballot(hit);
     if ((threadIdx.x & 63) == 0 && m) atomicAdd(out, (unsigned long long)__popcll(m));
@@ -386,8 +388,11 @@ extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_
         }
     // ctr: [0] status, [1] survivors, [2] candidates, [3] max count, [4] n_gt, [5] n_eq
     int rc = SCONE_OK;
-    const unsigned g_cap = (unsigned)((cap + kThreads - 1) / kThreads);
-    const unsigned g_bt = (unsigned)((BT + kThreads - 1) / kThreads);
+    // (The table clear covers up to 2^32 slots, more work-items than one
+    // launch holds; the other grids stay far below that at BT < 2^31.)
+    const int64_t g_cap = (int64_t)((cap + kThreads - 1) / kThreads);
+    const int64_t g_bt = (BT + kThreads - 1) / kThreads;
+    const dim3 block(kThreads);
     const int64_t waves_per_block = kThreads / 64;
     auto chunk_grid = [&](int64_t n) {
         const int64_t waves = (n + kChunk - 1) / kChunk;
@@ -397,7 +402,10 @@ extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_
     int32_t* ids_prev = ids_a;
     int32_t* ids_cur = ids_b;
     for (int n = 2; n <= max_len && rc == SCONE_OK; ++n) {
-        hipLaunchKernelGGL(k_table_clear, dim3(g_cap), dim3(kThreads), 0, st, table, cap);
+        if (launch_blocks(g_cap, kThreads, [&](int64_t b0, dim3 grid) {
+                hipLaunchKernelGGL(k_table_clear, grid, block, 0, st, table, cap, b0);
+            }) != hipSuccess)
+            rc = SCONE_EHIP;
         hipLaunchKernelGGL(k_count, dim3((unsigned)((BT + kCountPerBlock - 1) / kCountPerBlock)),
                            dim3(kThreads), 0, st, token_ids, BT, T, n,
                            ids_prev, table, mask, ctr + 0);
@@ -408,8 +416,11 @@ extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_
                            n < max_len ? skeys[n] : nullptr, ctr + 2, cand_key, cand_count,
                            cand_level, ctr + 3);
         if (n < max_len) {
-            hipLaunchKernelGGL(k_ids, dim3(g_bt), dim3(kThreads), 0, st, token_ids, BT, T, n,
-                               ids_prev, table, mask, ids_cur);
+            if (launch_blocks(g_bt, kThreads, [&](int64_t b0, dim3 grid) {
+                    hipLaunchKernelGGL(k_ids, grid, block, 0, st, token_ids, BT, T, n, ids_prev,
+                                       table, mask, ids_cur, b0);
+                }) != hipSuccess)
+                rc = SCONE_EHIP;
             int32_t* tmp = ids_prev;
             ids_prev = ids_cur;
             ids_cur = tmp;
@@ -428,9 +439,12 @@ extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_
     auto at_least = [&](uint32_t c, int64_t& out) -> bool {
         unsigned long long v = 0;
         if (hipMemsetAsync(acc, 0, sizeof(v), st) != hipSuccess) return false;
-        hipLaunchKernelGGL(k_count_at_least, dim3((unsigned)((n_cand + kThreads - 1) / kThreads)),
-                           dim3(kThreads), 0, st, cand_count, n_cand, c, acc);
-        if (hipMemcpyAsync(&v, acc, sizeof(v), hipMemcpyDeviceToHost, st) != hipSuccess ||
+        if (launch_blocks((n_cand + kThreads - 1) / kThreads, kThreads,
+                          [&](int64_t b0, dim3 grid) {
+                              hipLaunchKernelGGL(k_count_at_least, grid, dim3(kThreads), 0, st,
+                                                 cand_count, n_cand, c, acc, b0);
+                          }) != hipSuccess ||
+            hipMemcpyAsync(&v, acc, sizeof(v), hipMemcpyDeviceToHost, st) != hipSuccess ||
             hipStreamSynchronize(st) != hipSuccess)
             return false;
         out = (int64_t)v;

@@ -55,12 +55,14 @@ __global__ __launch_bounds__(kTileThreads) void k_embed(
     const typename SlotOps<SB>::Slot* __restrict__ slots, uint64_t mask,
     const int32_t* __restrict__ X, int64_t T, int P, int max_n, int64_t tiles_per_row,
     const V* __restrict__ rows, int64_t n_rows, int64_t upr, int shift, V* __restrict__ out,
-    int32_t* __restrict__ ids_out, int8_t* __restrict__ len_out, unsigned* __restrict__ err) {
+    int32_t* __restrict__ ids_out, int8_t* __restrict__ len_out, unsigned* __restrict__ err,
+    int64_t block0) {
     __shared__ int32_t s_tok[TileShape<G>::kPositions + kMaxHalo];
     __shared__ int32_t s_id[TileShape<G>::kPositions];
 
-    const int64_t b = blockIdx.x / tiles_per_row;
-    const int64_t t0 = (blockIdx.x - b * tiles_per_row) * (int64_t)P;
+    const int64_t blk = block_index(block0);
+    const int64_t b = blk / tiles_per_row;
+    const int64_t t0 = (blk - b * tiles_per_row) * (int64_t)P;
     stage_tokens(s_tok, X + b * T, T, t0, P, max_n - 1);
     __syncthreads();
     if (threadIdx.x < ((P * G + 63) & ~63)) {  // whole waves only
@@ -133,13 +135,12 @@ hipError_t launch(const scone_table* tb, const int32_t* X, int64_t B, int64_t T,
     int P = TileShape<G>::kPositions < 16 ? TileShape<G>::kPositions : 16;
     while (P > 4 && (int64_t)P * row_bytes > (32 << 10)) P >>= 1;
     const int64_t tiles = (T + P - 1) / P;
-    const int64_t grid = B * tiles;
-    if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((k_embed<SB, G, V, 4, kPow2>), dim3((unsigned)grid), dim3(kTileThreads),
-                       0, st, static_cast<const Slot*>(tb->slots), (uint64_t)tb->capacity - 1, X,
-                       T, P, max_n, tiles, static_cast<const V*>(rows), n_rows, upr, shift,
-                       static_cast<V*>(out), ids, lens, err);
-    return hipGetLastError();
+    return launch_blocks(B * tiles, kTileThreads, [&](int64_t b0, dim3 grid) {
+        hipLaunchKernelGGL((k_embed<SB, G, V, 4, kPow2>), grid, dim3(kTileThreads), 0, st,
+                           static_cast<const Slot*>(tb->slots), (uint64_t)tb->capacity - 1, X,
+                           T, P, max_n, tiles, static_cast<const V*>(rows), n_rows, upr, shift,
+                           static_cast<V*>(out), ids, lens, err, b0);
+    });
 }
 
 template <int SB, typename V, bool kPow2>

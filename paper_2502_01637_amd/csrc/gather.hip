@@ -22,8 +22,8 @@ constexpr int kGatherThreads = 256;
 template <typename V, int U, bool kPow2>
 __global__ __launch_bounds__(kGatherThreads) void k_gather(
     const int32_t* __restrict__ ids, int64_t total, const V* __restrict__ rows, int64_t n_rows,
-    int64_t upr, int shift, V* __restrict__ out, unsigned* __restrict__ err) {
-    const int64_t base = (int64_t)blockIdx.x * (kGatherThreads * U) + threadIdx.x;
+    int64_t upr, int shift, V* __restrict__ out, unsigned* __restrict__ err, int64_t block0) {
+    const int64_t base = block_index(block0) * (kGatherThreads * U) + threadIdx.x;
     V v[U];
     bool ok[U];
     if (base + (int64_t)(U - 1) * kGatherThreads < total) {
@@ -77,8 +77,8 @@ __global__ __launch_bounds__(kGatherThreads) void k_gather(
 template <int U>
 __global__ __launch_bounds__(kGatherThreads) void k_gather_rows(
     const int32_t* __restrict__ ids, int64_t n_tok, const u32x4* __restrict__ rows,
-    int64_t n_rows, u32x4* __restrict__ out, unsigned* __restrict__ err) {
-    const int64_t r = (int64_t)blockIdx.x * (kGatherThreads / 64) +
+    int64_t n_rows, u32x4* __restrict__ out, unsigned* __restrict__ err, int64_t block0) {
+    const int64_t r = block_index(block0) * (kGatherThreads / 64) +
                       __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (r >= n_tok) return;  // wave-uniform
     copy_row_wave<U>(ids, r, rows, n_rows, out, err);
@@ -87,10 +87,20 @@ __global__ __launch_bounds__(kGatherThreads) void k_gather_rows(
 // Every id is out of range when the table has no rows: zero the output.
 template <typename V>
 __global__ __launch_bounds__(kGatherThreads) void k_zero(int64_t total, V* __restrict__ out,
-                                                         unsigned* __restrict__ err) {
-    const int64_t i = (int64_t)blockIdx.x * kGatherThreads + threadIdx.x;
+                                                         unsigned* __restrict__ err,
+                                                         int64_t block0) {
+    const int64_t i = block_index(block0) * kGatherThreads + threadIdx.x;
     if (i < total) out[i] = V{};
     if (i == 0) atomicOr(err, err_bit(SCONE_EROW));
+}
+
+template <typename V>
+hipError_t launch_zero(int64_t total, V* out, unsigned* err, hipStream_t st) {
+    return launch_blocks((total + kGatherThreads - 1) / kGatherThreads, kGatherThreads,
+                         [&](int64_t b0, dim3 grid) {
+                             hipLaunchKernelGGL(k_zero<V>, grid, dim3(kGatherThreads), 0, st,
+                                                total, out, err, b0);
+                         });
 }
 
 template <typename V, int U>
@@ -98,37 +108,27 @@ hipError_t launch_gather(const int32_t* ids, int64_t n_tok, const void* rows, in
                          int64_t row_bytes, void* out, unsigned* err, hipStream_t st) {
     const int64_t upr = row_bytes / (int64_t)sizeof(V);
     const int64_t total = n_tok * upr;
-    const int64_t grid = (total + kGatherThreads * U - 1) / (kGatherThreads * U);
-    if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    if (n_rows == 0) {
-        const int64_t zgrid = (total + kGatherThreads - 1) / kGatherThreads;
-        if (zgrid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-        hipLaunchKernelGGL(k_zero<V>, dim3((unsigned)zgrid), dim3(kGatherThreads), 0, st, total,
-                           static_cast<V*>(out), err);
-        return hipGetLastError();
-    }
+    if (n_rows == 0) return launch_zero(total, static_cast<V*>(out), err, st);
+    const int64_t blocks = (total + kGatherThreads * U - 1) / (kGatherThreads * U);
     const bool pow2 = (upr & (upr - 1)) == 0;
     int shift = 0;
     while (((int64_t)1 << shift) < upr) ++shift;
-    if (pow2)
-        hipLaunchKernelGGL((k_gather<V, U, true>), dim3((unsigned)grid), dim3(kGatherThreads), 0,
-                           st, ids, total, static_cast<const V*>(rows), n_rows, upr, shift,
-                           static_cast<V*>(out), err);
-    else
-        hipLaunchKernelGGL((k_gather<V, U, false>), dim3((unsigned)grid), dim3(kGatherThreads),
-                           0, st, ids, total, static_cast<const V*>(rows), n_rows, upr, shift,
-                           static_cast<V*>(out), err);
-    return hipGetLastError();
+    return launch_blocks(blocks, kGatherThreads, [&](int64_t b0, dim3 grid) {
+        if (pow2)
+            hipLaunchKernelGGL((k_gather<V, U, true>), grid, dim3(kGatherThreads), 0, st, ids,
+                               total, static_cast<const V*>(rows), n_rows, upr, shift,
+                               static_cast<V*>(out), err, b0);
+        else
+            hipLaunchKernelGGL((k_gather<V, U, false>), grid, dim3(kGatherThreads), 0, st, ids,
+                               total, static_cast<const V*>(rows), n_rows, upr, shift,
+                               static_cast<V*>(out), err, b0);
+    });
 }
 
 }  // namespace
 
 hipError_t launch_zero_rows(void* out, int64_t bytes, unsigned* err, hipStream_t st) {
-    const int64_t grid = (bytes + kGatherThreads - 1) / kGatherThreads;
-    if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(k_zero<uint8_t>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, bytes,
-                       static_cast<uint8_t*>(out), err);
-    return hipGetLastError();
+    return launch_zero(bytes, static_cast<uint8_t*>(out), err, st);
 }
 
 hipError_t launch_gather_any(const int32_t* ids, int64_t n_tok, const void* rows, int64_t n_rows,
@@ -138,17 +138,18 @@ hipError_t launch_gather_any(const int32_t* ids, int64_t n_tok, const void* rows
     const int64_t upr16 = row_bytes / 16;
     if ((align & 15) == 0 && n_rows > 0 &&
         (upr16 == 64 || upr16 == 128 || upr16 == 256 || upr16 == 512)) {
-        const int64_t grid = (n_tok + kGatherThreads / 64 - 1) / (kGatherThreads / 64);
-        if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+        const int64_t blocks = (n_tok + kGatherThreads / 64 - 1) / (kGatherThreads / 64);
         const u32x4* R = static_cast<const u32x4*>(rows);
         u32x4* O = static_cast<u32x4*>(out);
-        switch (upr16) {
-            case 64: hipLaunchKernelGGL(k_gather_rows<1>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, ids, n_tok, R, n_rows, O, err); break;
-            case 128: hipLaunchKernelGGL(k_gather_rows<2>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, ids, n_tok, R, n_rows, O, err); break;
-            case 256: hipLaunchKernelGGL(k_gather_rows<4>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, ids, n_tok, R, n_rows, O, err); break;
-            default: hipLaunchKernelGGL(k_gather_rows<8>, dim3((unsigned)grid), dim3(kGatherThreads), 0, st, ids, n_tok, R, n_rows, O, err); break;
-        }
-        return hipGetLastError();
+        return launch_blocks(blocks, kGatherThreads, [&](int64_t b0, dim3 grid) {
+            const dim3 block(kGatherThreads);
+            switch (upr16) {
+                case 64: hipLaunchKernelGGL(k_gather_rows<1>, grid, block, 0, st, ids, n_tok, R, n_rows, O, err, b0); break;
+                case 128: hipLaunchKernelGGL(k_gather_rows<2>, grid, block, 0, st, ids, n_tok, R, n_rows, O, err, b0); break;
+                case 256: hipLaunchKernelGGL(k_gather_rows<4>, grid, block, 0, st, ids, n_tok, R, n_rows, O, err, b0); break;
+                default: hipLaunchKernelGGL(k_gather_rows<8>, grid, block, 0, st, ids, n_tok, R, n_rows, O, err, b0); break;
+            }
+        });
     }
     if ((align & 15) == 0)
         return launch_gather<u32x4, 4>(ids, n_tok, rows, n_rows, row_bytes, out, err, st);

@@ -27,8 +27,8 @@ __device__ __forceinline__ uint64_t id_hash(int32_t id) {
 }
 
 __global__ __launch_bounds__(kThreads) void k_split_clear(int32_t* keys, uint64_t cap,
-                                                          unsigned* count) {
-    const uint64_t i = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
+                                                          unsigned* count, int64_t block0) {
+    const uint64_t i = (uint64_t)block_index(block0) * kThreads + threadIdx.x;
     if (i < cap) keys[i] = kEmpty;
     if (i == 0) *count = 0;
 }
@@ -36,8 +36,8 @@ __global__ __launch_bounds__(kThreads) void k_split_clear(int32_t* keys, uint64_
 __global__ __launch_bounds__(kThreads) void k_split_insert(const int32_t* __restrict__ ids,
                                                            int64_t n_tok, int64_t n_near,
                                                            int64_t n_far, int32_t* keys,
-                                                           uint64_t mask) {
-    const int64_t k = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+                                                           uint64_t mask, int64_t block0) {
+    const int64_t k = block_index(block0) * kThreads + threadIdx.x;
     if (k >= n_tok) return;
     const int32_t id = ids[k];
     if ((int64_t)id < n_near || (int64_t)id >= n_near + n_far) return;  // near or bad
@@ -52,8 +52,9 @@ __global__ __launch_bounds__(kThreads) void k_split_insert(const int32_t* __rest
 __global__ __launch_bounds__(kThreads) void k_split_number(const int32_t* __restrict__ keys,
                                                            int32_t* __restrict__ index,
                                                            int32_t* __restrict__ unique,
-                                                           uint64_t cap, unsigned* count) {
-    const uint64_t s = (uint64_t)blockIdx.x * kThreads + threadIdx.x;
+                                                           uint64_t cap, unsigned* count,
+                                                           int64_t block0) {
+    const uint64_t s = (uint64_t)block_index(block0) * kThreads + threadIdx.x;
     if (s >= cap) return;
     const int32_t id = keys[s];
     if (id == kEmpty) return;
@@ -67,8 +68,9 @@ __global__ __launch_bounds__(kThreads) void k_split_fetch(const int32_t* __restr
                                                           const unsigned* __restrict__ count,
                                                           int64_t n_near, const u32x4* far,
                                                           int64_t upr, u32x4* __restrict__ staging,
-                                                          int32_t* __restrict__ n_unique) {
-    const int64_t u = (int64_t)blockIdx.x * (kThreads / 64) +
+                                                          int32_t* __restrict__ n_unique,
+                                                          int64_t block0) {
+    const int64_t u = block_index(block0) * (kThreads / 64) +
                       __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const unsigned total = *count;
     if (u == 0 && threadIdx.x == 0 && n_unique) *n_unique = (int32_t)total;
@@ -92,8 +94,8 @@ __global__ __launch_bounds__(kThreads) void k_split_gather(
     const int32_t* __restrict__ ids, int64_t n_tok, const u32x4* __restrict__ near,
     int64_t n_near, int64_t n_far, const int32_t* __restrict__ keys,
     const int32_t* __restrict__ index, uint64_t mask, const u32x4* __restrict__ staging,
-    int64_t upr, u32x4* __restrict__ out, unsigned* __restrict__ err) {
-    const int64_t r = (int64_t)blockIdx.x * (kThreads / 64) +
+    int64_t upr, u32x4* __restrict__ out, unsigned* __restrict__ err, int64_t block0) {
+    const int64_t r = block_index(block0) * (kThreads / 64) +
                       __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (r >= n_tok) return;  // wave-uniform
     const int lane = threadIdx.x & 63;
@@ -189,18 +191,33 @@ extern "C" int scone_gather_split(const int32_t* fgram_ids, int64_t n_tok, const
     u32x4* staging = reinterpret_cast<u32x4*>(ws + l.staging);
     const int64_t upr = row_bytes / 16;
     const uint64_t mask = l.cap - 1;
-    const unsigned g_cap = (unsigned)((l.cap + kThreads - 1) / kThreads);
-    const unsigned g_tok = (unsigned)((n_tok + kThreads - 1) / kThreads);
-    const unsigned g_rows = (unsigned)((n_tok + 3) / 4);
-    hipLaunchKernelGGL(k_split_clear, dim3(g_cap), dim3(kThreads), 0, st, keys, l.cap, count);
-    hipLaunchKernelGGL(k_split_insert, dim3(g_tok), dim3(kThreads), 0, st, fgram_ids, n_tok,
-                       n_near, n_far, keys, mask);
-    hipLaunchKernelGGL(k_split_number, dim3(g_cap), dim3(kThreads), 0, st, keys, index, unique,
-                       l.cap, count);
-    hipLaunchKernelGGL(k_split_fetch, dim3(g_rows), dim3(kThreads), 0, st, unique, count, n_near,
-                       static_cast<const u32x4*>(far_rows), upr, staging, n_unique);
-    hipLaunchKernelGGL(k_split_gather, dim3(g_rows), dim3(kThreads), 0, st, fgram_ids, n_tok,
-                       static_cast<const u32x4*>(near_rows), n_near, n_far, keys, index, mask,
-                       staging, upr, static_cast<u32x4*>(out), err);
-    return hipGetLastError() == hipSuccess ? SCONE_OK : SCONE_EHIP;
+    const int64_t g_cap = ((int64_t)l.cap + kThreads - 1) / kThreads;
+    const int64_t g_tok = (n_tok + kThreads - 1) / kThreads;
+    const int64_t g_rows = (n_tok + 3) / 4;
+    const dim3 block(kThreads);
+    hipError_t e = launch_blocks(g_cap, kThreads, [&](int64_t b0, dim3 grid) {
+        hipLaunchKernelGGL(k_split_clear, grid, block, 0, st, keys, l.cap, count, b0);
+    });
+    if (e == hipSuccess)
+        e = launch_blocks(g_tok, kThreads, [&](int64_t b0, dim3 grid) {
+            hipLaunchKernelGGL(k_split_insert, grid, block, 0, st, fgram_ids, n_tok, n_near,
+                               n_far, keys, mask, b0);
+        });
+    if (e == hipSuccess)
+        e = launch_blocks(g_cap, kThreads, [&](int64_t b0, dim3 grid) {
+            hipLaunchKernelGGL(k_split_number, grid, block, 0, st, keys, index, unique, l.cap,
+                               count, b0);
+        });
+    if (e == hipSuccess)
+        e = launch_blocks(g_rows, kThreads, [&](int64_t b0, dim3 grid) {
+            hipLaunchKernelGGL(k_split_fetch, grid, block, 0, st, unique, count, n_near,
+                               static_cast<const u32x4*>(far_rows), upr, staging, n_unique, b0);
+        });
+    if (e == hipSuccess)
+        e = launch_blocks(g_rows, kThreads, [&](int64_t b0, dim3 grid) {
+            hipLaunchKernelGGL(k_split_gather, grid, block, 0, st, fgram_ids, n_tok,
+                               static_cast<const u32x4*>(near_rows), n_near, n_far, keys, index,
+                               mask, staging, upr, static_cast<u32x4*>(out), err, b0);
+        });
+    return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
 }

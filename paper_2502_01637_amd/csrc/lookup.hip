@@ -19,13 +19,13 @@ __global__ __launch_bounds__(kTileThreads) void k_lookup(
     const typename SlotOps<SB>::Slot* __restrict__ slots, uint64_t mask,
     const int32_t* __restrict__ X, int64_t T, int max_n, int64_t tiles_per_row,
     int32_t* __restrict__ ids_out, int8_t* __restrict__ len_out,
-    unsigned long long* __restrict__ hist, unsigned* __restrict__ err) {
+    unsigned long long* __restrict__ hist, unsigned* __restrict__ err, int64_t block0) {
     constexpr int P = TileShape<G>::kPositions;
     __shared__ int32_t s_tok[P + kMaxHalo];
     __shared__ unsigned s_hist[SCONE_MAX_FGRAM_LEN + 1];
     if (hist && threadIdx.x <= SCONE_MAX_FGRAM_LEN) s_hist[threadIdx.x] = 0;
-    const int len = lookup_block<SB, G>(slots, mask, X, T, max_n, tiles_per_row, blockIdx.x,
-                                        s_tok, ids_out, len_out, err);
+    const int len = lookup_block<SB, G>(slots, mask, X, T, max_n, tiles_per_row,
+                                        block_index(block0), s_tok, ids_out, len_out, err);
     if (hist && len) atomicAdd(&s_hist[len], 1u);
     if (hist) {  // uniform: the whole workgroup takes this branch or none does
         __syncthreads();
@@ -41,12 +41,11 @@ hipError_t launch(const scone_table* tb, const int32_t* X, int64_t B, int64_t T,
     using Slot = typename SlotOps<SB>::Slot;
     constexpr int P = TileShape<G>::kPositions;
     const int64_t tiles = (T + P - 1) / P;
-    const int64_t grid = B * tiles;
-    if (grid > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((k_lookup<SB, G>), dim3((unsigned)grid), dim3(kTileThreads), 0, st,
-                       static_cast<const Slot*>(tb->slots), (uint64_t)tb->capacity - 1, X, T,
-                       max_n, tiles, ids, lens, hist, err);
-    return hipGetLastError();
+    return launch_blocks(B * tiles, kTileThreads, [&](int64_t b0, dim3 grid) {
+        hipLaunchKernelGGL((k_lookup<SB, G>), grid, dim3(kTileThreads), 0, st,
+                           static_cast<const Slot*>(tb->slots), (uint64_t)tb->capacity - 1, X, T,
+                           max_n, tiles, ids, lens, hist, err, b0);
+    });
 }
 
 template <int SB>

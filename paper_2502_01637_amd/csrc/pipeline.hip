@@ -24,14 +24,15 @@ __global__ __launch_bounds__(kTileThreads) void k_pipelined(
     const int32_t* __restrict__ X, int64_t T, int max_n, int64_t tiles_per_row,
     int64_t n_lookup_blocks, int32_t* __restrict__ next_ids, int8_t* __restrict__ next_len,
     const int32_t* __restrict__ cur_ids, int64_t n_cur, const u32x4* __restrict__ rows,
-    int64_t n_rows, u32x4* __restrict__ out, unsigned* __restrict__ err) {
+    int64_t n_rows, u32x4* __restrict__ out, unsigned* __restrict__ err, int64_t block0) {
     __shared__ int32_t s_tok[TileShape<G>::kPositions + kMaxHalo];
-    if ((int64_t)blockIdx.x < n_lookup_blocks) {  // workgroup-uniform
-        lookup_block<SB, G>(slots, mask, X, T, max_n, tiles_per_row, blockIdx.x, s_tok,
-                            next_ids, next_len, err);
+    const int64_t blk = block_index(block0);
+    if (blk < n_lookup_blocks) {  // workgroup-uniform
+        lookup_block<SB, G>(slots, mask, X, T, max_n, tiles_per_row, blk, s_tok, next_ids,
+                            next_len, err);
         return;
     }
-    const int64_t r = ((int64_t)blockIdx.x - n_lookup_blocks) * (kTileThreads / 64) +
+    const int64_t r = (blk - n_lookup_blocks) * (kTileThreads / 64) +
                       __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (r >= n_cur) return;  // wave-uniform
     copy_row_wave<U>(cur_ids, r, rows, n_rows, out, err);
@@ -60,14 +61,13 @@ hipError_t launch(const Step& s) {
     const int64_t tiles = (s.T + P - 1) / P;
     const int64_t n_lookup = s.B * tiles;
     const int64_t n_gather = (s.n_cur + kTileThreads / 64 - 1) / (kTileThreads / 64);
-    if (n_lookup + n_gather > 0x7fffffffLL) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((k_pipelined<SB, G, U>), dim3((unsigned)(n_lookup + n_gather)),
-                       dim3(kTileThreads), 0, s.st, static_cast<const Slot*>(s.tb->slots),
-                       (uint64_t)s.tb->capacity - 1, s.X, s.T, s.max_n, tiles, n_lookup,
-                       s.next_ids, s.next_len, s.cur_ids, s.n_cur,
-                       static_cast<const u32x4*>(s.rows), s.n_rows, static_cast<u32x4*>(s.out),
-                       s.err);
-    return hipGetLastError();
+    return launch_blocks(n_lookup + n_gather, kTileThreads, [&](int64_t b0, dim3 grid) {
+        hipLaunchKernelGGL((k_pipelined<SB, G, U>), grid, dim3(kTileThreads), 0, s.st,
+                           static_cast<const Slot*>(s.tb->slots), (uint64_t)s.tb->capacity - 1,
+                           s.X, s.T, s.max_n, tiles, n_lookup, s.next_ids, s.next_len,
+                           s.cur_ids, s.n_cur, static_cast<const u32x4*>(s.rows), s.n_rows,
+                           static_cast<u32x4*>(s.out), s.err, b0);
+    });
 }
 
 template <int SB, int G>

@@ -24,6 +24,35 @@ unsigned* device_error_word();
         if ((expr) != hipSuccess) return SCONE_EHIP;       \
     } while (0)
 
+// ------------------------------------------------------------- launches ----
+// A dispatch states its grid as a count of work-items held in 32 bits per
+// dimension, so a one-dimensional launch of 2^32 work-items or more would
+// wrap around and run only the remainder, without an error.  Every kernel
+// therefore takes the index of its first workgroup, `block0`, and launches go
+// through launch_blocks, which issues consecutive launches of at most
+// kMaxLaunchItems work-items each.
+
+constexpr int64_t kMaxLaunchItems = (int64_t)1 << 31;
+
+// Issues `blocks` workgroups of `threads` work-items: one(b0, grid) launches
+// workgroups b0 .. b0 + grid.x - 1.  Returns the first launch error.
+template <typename F>
+hipError_t launch_blocks(int64_t blocks, int threads, F&& one) {
+    const int64_t per = kMaxLaunchItems / threads;
+    for (int64_t b0 = 0; b0 < blocks; b0 += per) {
+        const int64_t n = blocks - b0 < per ? blocks - b0 : per;
+        one(b0, dim3((unsigned)n));
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+// This workgroup's index in the whole grid of a launch_blocks call.
+__device__ __forceinline__ int64_t block_index(int64_t block0) {
+    return block0 + (int64_t)blockIdx.x;
+}
+
 // ---------------------------------------------------------- f-gram keys ----
 // An f-gram of n <= 7 tokens, each < 2^16, is one bit string:
 //   bits [0, 4)              the length n

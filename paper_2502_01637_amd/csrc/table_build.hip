@@ -32,8 +32,8 @@ __global__ __launch_bounds__(kBuildThreads) void k_insert(
     const int32_t* __restrict__ fgrams, const int32_t* __restrict__ lengths,
     const int32_t* __restrict__ ids, int64_t n, int max_len,
     typename SlotOps<SB>::Slot* __restrict__ slots, uint64_t mask,
-    int64_t* __restrict__ slot_of, unsigned* __restrict__ status) {
-    const int64_t k = (int64_t)blockIdx.x * kBuildThreads + threadIdx.x;
+    int64_t* __restrict__ slot_of, unsigned* __restrict__ status, int64_t block0) {
+    const int64_t k = block_index(block0) * kBuildThreads + threadIdx.x;
     if (k >= n) return;
     slot_of[k] = -1;
     const int len = lengths[k];
@@ -69,8 +69,8 @@ template <int SB>
 __global__ __launch_bounds__(kBuildThreads) void k_verify(
     const int32_t* __restrict__ fgrams, const int32_t* __restrict__ lengths, int64_t n,
     int max_len, const typename SlotOps<SB>::Slot* __restrict__ slots, uint64_t mask,
-    const int64_t* __restrict__ slot_of, unsigned* __restrict__ status) {
-    const int64_t k = (int64_t)blockIdx.x * kBuildThreads + threadIdx.x;
+    const int64_t* __restrict__ slot_of, unsigned* __restrict__ status, int64_t block0) {
+    const int64_t k = block_index(block0) * kBuildThreads + threadIdx.x;
     if (k >= n) return;
     const int64_t mine = slot_of[k];
     if (mine < 0) return;  // rejected or not placed: already reported
@@ -96,14 +96,16 @@ hipError_t launch_build(const int32_t* fgrams, const int32_t* lengths, const int
                         int64_t n, int max_len, void* slots, uint64_t mask, int64_t* slot_of,
                         unsigned* status, hipStream_t st) {
     using Slot = typename SlotOps<SB>::Slot;
-    const unsigned grid = (unsigned)((n + kBuildThreads - 1) / kBuildThreads);
-    hipLaunchKernelGGL(k_insert<SB>, dim3(grid), dim3(kBuildThreads), 0, st, fgrams, lengths,
-                       ids, n, max_len, static_cast<Slot*>(slots), mask, slot_of, status);
-    hipError_t e = hipGetLastError();
+    const int64_t blocks = (n + kBuildThreads - 1) / kBuildThreads;
+    const hipError_t e = launch_blocks(blocks, kBuildThreads, [&](int64_t b0, dim3 grid) {
+        hipLaunchKernelGGL(k_insert<SB>, grid, dim3(kBuildThreads), 0, st, fgrams, lengths, ids,
+                           n, max_len, static_cast<Slot*>(slots), mask, slot_of, status, b0);
+    });
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_verify<SB>, dim3(grid), dim3(kBuildThreads), 0, st, fgrams, lengths, n,
-                       max_len, static_cast<const Slot*>(slots), mask, slot_of, status);
-    return hipGetLastError();
+    return launch_blocks(blocks, kBuildThreads, [&](int64_t b0, dim3 grid) {
+        hipLaunchKernelGGL(k_verify<SB>, grid, dim3(kBuildThreads), 0, st, fgrams, lengths, n,
+                           max_len, static_cast<const Slot*>(slots), mask, slot_of, status, b0);
+    });
 }
 
 }  // namespace
@@ -124,8 +126,6 @@ extern "C" int scone_build_fgram_table(const int32_t* fgrams, const int32_t* len
     uint64_t cap = 64;
     while ((double)cap < want) cap <<= 1;
     const int slot_bytes = max_len <= kMaxLenSlot16 ? 16 : 32;
-    const unsigned grid = (unsigned)((n + 255) / 256);
-    if ((uint64_t)grid > 0x7fffffffull) return SCONE_EINVAL;
 
     hipStream_t st = static_cast<hipStream_t>(stream);
     int dev = 0;
