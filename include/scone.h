@@ -275,7 +275,8 @@ int64_t scone_gather_split_workspace(int64_t n_tok, int64_t row_bytes);
  * n-grams never cross from one sequence into the next.
  *
  *  token_ids  [B, T] int32 (each in [0, SCONE_TOKEN_LIMIT), else
- *             SCONE_ETOKEN); B * T < 2^31.
+ *             SCONE_ETOKEN); B * T < 2^31 and (max_len - 1) * B * T < 2^32
+ *             (candidates are counted in 32 bits), else SCONE_EINVAL.
  *  max_len    K, in [2, SCONE_MAX_FGRAM_LEN].
  *  S          the number of f-grams wanted.
  *  fgrams     [S, max_len] int32 output, row k holding f-gram k oldest first,

@@ -341,6 +341,8 @@ extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_
     if (B > 0 && T > ((int64_t)1 << 40) / B) return SCONE_EINVAL;
     const int64_t BT = B * T;
     if (BT >= ((int64_t)1 << 31)) return SCONE_EINVAL;  // dense ids and counters are 32-bit
+    // every candidate of every scan is counted in one 32-bit counter
+    if (BT * (int64_t)(max_len - 1) >= ((int64_t)1 << 32)) return SCONE_EINVAL;
     if (BT == 0 || S == 0) return SCONE_OK;
     if (!token_ids || !fgrams || !lengths || !counts) return SCONE_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
