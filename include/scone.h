@@ -25,8 +25,9 @@
  *    contents of the outputs are unspecified.
  *  - No call allocates device memory except scone_build_fgram_table,
  *    scone_host_alloc and the synchronous offline calls
- *    scone_discover_fgrams and scone_fgram_model_forward (and a 4-byte error
- *    word per device on first use).
+ *    scone_discover_fgrams (when given no workspace) and
+ *    scone_fgram_model_forward (and a 4-byte error word per device on first
+ *    use).
  *  - All buffers are owned by the caller except the table handle, which the
  *    library owns until scone_table_destroy.
  */
@@ -283,14 +284,26 @@ int64_t scone_gather_split_workspace(int64_t n_tok, int64_t row_bytes);
  *             padded with -1; lengths [S] and counts [S] int32 outputs.
  *  n_found    host pointer receiving min(S, number of candidates); only that
  *             many rows are written.
+ *  workspace  device scratch of at least scone_discover_workspace(B, T,
+ *             max_len) bytes, 256-byte aligned, caller-owned and reusable
+ *             across calls that do not overlap (else SCONE_EINVAL); or NULL,
+ *             and the call allocates that much itself and frees it before
+ *             returning.
  *
  * The output is ready for scone_build_fgram_table (ids are the caller's
- * choice).  Synchronous; allocates and frees its own device scratch
- * (about 16 * 2 * B * T bytes of counting table plus per-scan arrays).
+ * choice).  Synchronous (it reads the candidate count and a count histogram
+ * back to choose the top-S threshold).
  */
 int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_t T, int32_t max_len,
                           int32_t min_count, int64_t S, int32_t* fgrams, int32_t* lengths,
-                          int32_t* counts, int64_t* n_found, void* stream);
+                          int32_t* counts, int64_t* n_found, void* workspace,
+                          int64_t workspace_bytes, void* stream);
+
+/* Bytes of workspace scone_discover_fgrams needs for a [B, T] corpus and
+ * f-grams up to max_len tokens (a counting table of 16-byte slots, at least
+ * 2 B T of them, plus about (13 (max_len - 1) + 8 (max_len - 2) + 8) B T
+ * bytes of per-scan arrays), or -1 for sizes the call rejects. */
+int64_t scone_discover_workspace(int64_t B, int64_t T, int32_t max_len);
 
 /*
  * Precompute the f-gram embedding layer (Section 3.2: F caches the f-gram

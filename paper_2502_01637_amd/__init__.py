@@ -9,9 +9,11 @@ from . import scone
 from .scone import (SconeError, Table, HostRows, build_fgram_table, lookup, gather, embed,
                     embed_pipelined,
                     decode_step, gather_split, split_workspace_bytes, tag, discover_fgrams,
+                    discover_workspace_bytes,
                     FgramModel, precompute_fgram_rows, check, check_ok)
 
 __all__ = ["scone", "SconeError", "Table", "HostRows", "build_fgram_table", "lookup", "gather",
            "embed", "embed_pipelined", "decode_step", "gather_split", "split_workspace_bytes", "tag", "discover_fgrams",
+           "discover_workspace_bytes",
            "FgramModel", "precompute_fgram_rows", "check",
            "check_ok"]

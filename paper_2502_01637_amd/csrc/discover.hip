@@ -329,65 +329,118 @@ __global__ __launch_bounds__(kThreads) void k_select(
 }  // namespace
 }  // namespace scone
 
-extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_t T,
-                                     int32_t max_len, int32_t min_count, int64_t S,
-                                     int32_t* fgrams, int32_t* lengths, int32_t* counts,
-                                     int64_t* n_found, void* stream) {
-    using namespace scone;
-    if (!n_found) return SCONE_EINVAL;
-    *n_found = 0;
-    if (B < 0 || T < 0 || S < 0 || min_count < 1) return SCONE_EINVAL;
+namespace scone {
+namespace {
+
+// Scratch of one call, carved from one workspace: the counting table, the
+// dense ids of two consecutive scans, the candidates, the counters and
+// histogram, and the survivors' codes of every scan but the last.
+struct DiscLayout {
+    uint64_t cap;
+    int64_t cand_cap;
+    size_t table, ids_a, ids_b, cand_key, cand_count, cand_level, ctr, acc, hist;
+    size_t skey[SCONE_MAX_FGRAM_LEN + 1];
+    size_t total;
+};
+
+DiscLayout disc_layout(int64_t BT, int max_len) {
+    DiscLayout l{};
+    l.cap = 64;
+    while ((int64_t)l.cap < 2 * BT) l.cap <<= 1;
+    l.cand_cap = BT * (int64_t)(max_len - 1);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off = (off + bytes + 255) & ~(size_t)255;
+        return at;
+    };
+    l.table = take(l.cap * sizeof(CountSlot));
+    l.ids_a = take(BT * sizeof(int32_t));
+    l.ids_b = take(BT * sizeof(int32_t));
+    l.cand_key = take(l.cand_cap * sizeof(uint64_t));
+    l.cand_count = take(l.cand_cap * sizeof(uint32_t));
+    l.cand_level = take(l.cand_cap);
+    l.ctr = take(16 * sizeof(unsigned));
+    l.acc = take(sizeof(unsigned long long));
+    l.hist = take(kHistBins * sizeof(unsigned long long));
+    for (int L = 2; L < max_len; ++L) l.skey[L] = take(BT * sizeof(uint64_t));
+    l.total = off;
+    return l;
+}
+
+// SCONE_OK when (B, T, max_len) are sizes the call handles.
+int disc_sizes_ok(int64_t B, int64_t T, int32_t max_len) {
+    if (B < 0 || T < 0) return SCONE_EINVAL;
     if (max_len < 2 || max_len > SCONE_MAX_FGRAM_LEN) return SCONE_EINVAL;
     if (B > 0 && T > ((int64_t)1 << 40) / B) return SCONE_EINVAL;
     const int64_t BT = B * T;
     if (BT >= ((int64_t)1 << 31)) return SCONE_EINVAL;  // dense ids and counters are 32-bit
     // every candidate of every scan is counted in one 32-bit counter
     if (BT * (int64_t)(max_len - 1) >= ((int64_t)1 << 32)) return SCONE_EINVAL;
+    return SCONE_OK;
+}
+
+}  // namespace
+}  // namespace scone
+
+extern "C" int64_t scone_discover_workspace(int64_t B, int64_t T, int32_t max_len) {
+    using namespace scone;
+    if (disc_sizes_ok(B, T, max_len) != SCONE_OK) return -1;
+    return (int64_t)disc_layout(B * T, max_len).total;
+}
+
+extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_t T,
+                                     int32_t max_len, int32_t min_count, int64_t S,
+                                     int32_t* fgrams, int32_t* lengths, int32_t* counts,
+                                     int64_t* n_found, void* workspace, int64_t workspace_bytes,
+                                     void* stream) {
+    using namespace scone;
+    if (!n_found) return SCONE_EINVAL;
+    *n_found = 0;
+    if (S < 0 || min_count < 1) return SCONE_EINVAL;
+    if (disc_sizes_ok(B, T, max_len) != SCONE_OK) return SCONE_EINVAL;
+    const int64_t BT = B * T;
     if (BT == 0 || S == 0) return SCONE_OK;
     if (!token_ids || !fgrams || !lengths || !counts) return SCONE_EINVAL;
+    const DiscLayout lay = disc_layout(BT, max_len);
+    if (workspace && (workspace_bytes < 0 || (uint64_t)workspace_bytes < lay.total))
+        return SCONE_EINVAL;
+    if ((uintptr_t)workspace % 256 != 0) return SCONE_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
 
-    uint64_t cap = 64;
-    while ((int64_t)cap < 2 * BT) cap <<= 1;
+    const uint64_t cap = lay.cap;
     const uint64_t mask = cap - 1;
-    const int64_t cand_cap = BT * (int64_t)(max_len - 1);
 
-    // Device scratch, freed before returning (the call is synchronous).
-    std::vector<void*> allocs;
-    auto grab = [&](size_t bytes) -> void* {
-        void* p = nullptr;
-        if (hipMalloc(&p, bytes ? bytes : 16) != hipSuccess) {
+    // Without a workspace the call takes its scratch in one allocation and
+    // frees it before returning (the call is synchronous).
+    void* own = nullptr;
+    if (!workspace) {
+        if (hipMalloc(&own, lay.total) != hipSuccess) {
             (void)hipGetLastError();
-            return nullptr;
+            return SCONE_ENOMEM;
         }
-        allocs.push_back(p);
-        return p;
-    };
+        workspace = own;
+    }
     auto release = [&]() {
         (void)hipStreamSynchronize(st);
-        for (void* p : allocs) (void)hipFree(p);
+        if (own) (void)hipFree(own);
     };
-    CountSlot* table = static_cast<CountSlot*>(grab(cap * sizeof(CountSlot)));
-    int32_t* ids_a = static_cast<int32_t*>(grab(BT * sizeof(int32_t)));
-    int32_t* ids_b = static_cast<int32_t*>(grab(BT * sizeof(int32_t)));
-    uint64_t* cand_key = static_cast<uint64_t*>(grab(cand_cap * sizeof(uint64_t)));
-    uint32_t* cand_count = static_cast<uint32_t*>(grab(cand_cap * sizeof(uint32_t)));
-    int8_t* cand_level = static_cast<int8_t*>(grab(cand_cap));
-    unsigned* ctr = static_cast<unsigned*>(grab(16 * sizeof(unsigned)));
-    unsigned long long* acc = static_cast<unsigned long long*>(grab(sizeof(unsigned long long)));
-    unsigned long long* hist =
-        static_cast<unsigned long long*>(grab(kHistBins * sizeof(unsigned long long)));
+    uint8_t* ws = static_cast<uint8_t*>(workspace);
+    CountSlot* table = reinterpret_cast<CountSlot*>(ws + lay.table);
+    int32_t* ids_a = reinterpret_cast<int32_t*>(ws + lay.ids_a);
+    int32_t* ids_b = reinterpret_cast<int32_t*>(ws + lay.ids_b);
+    uint64_t* cand_key = reinterpret_cast<uint64_t*>(ws + lay.cand_key);
+    uint32_t* cand_count = reinterpret_cast<uint32_t*>(ws + lay.cand_count);
+    int8_t* cand_level = reinterpret_cast<int8_t*>(ws + lay.cand_level);
+    unsigned* ctr = reinterpret_cast<unsigned*>(ws + lay.ctr);
+    unsigned long long* acc = reinterpret_cast<unsigned long long*>(ws + lay.acc);
+    unsigned long long* hist = reinterpret_cast<unsigned long long*>(ws + lay.hist);
     LevelKeys lk{};
     uint64_t* skeys[SCONE_MAX_FGRAM_LEN + 1] = {};
     for (int L = 2; L < max_len; ++L) {
-        skeys[L] = static_cast<uint64_t*>(grab(BT * sizeof(uint64_t)));
+        skeys[L] = reinterpret_cast<uint64_t*>(ws + lay.skey[L]);
         lk.skey[L] = skeys[L];
     }
-    for (void* p : allocs)
-        if (!p) {
-            release();
-            return SCONE_ENOMEM;
-        }
     // ctr: [0] status, [1] survivors, [2] candidates, [3] max count, [4] n_gt, [5] n_eq
     int rc = SCONE_OK;
     // (The table clear covers up to 2^32 slots, more work-items than one

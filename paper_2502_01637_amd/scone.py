@@ -51,7 +51,9 @@ def _declare(L):
     L.scone_decode_step.argtypes = [P, P, P, I32, P, I64, I32, P, I64, I64, I32, P, P, P, P]
     L.scone_decode_step.restype = I
     L.scone_discover_fgrams.argtypes = [P, I64, I64, I32, I32, I64, P, P, P,
-                                        ctypes.POINTER(I64), P]
+                                        ctypes.POINTER(I64), P, I64, P]
+    L.scone_discover_workspace.argtypes = [I64, I64, I32]
+    L.scone_discover_workspace.restype = I64
     L.scone_discover_fgrams.restype = I
     L.scone_tag.argtypes = [P, P, I64, I64, I32, P, P, P]
     L.scone_tag.restype = I
@@ -217,14 +219,28 @@ def tag(table: Table, token_ids: torch.Tensor, max_n: int,
     return match_len, hist
 
 
+def discover_workspace_bytes(B: int, T: int, max_len: int) -> int:
+    """Bytes of scratch scone_discover_fgrams needs (-1 for rejected sizes)."""
+    return int(lib().scone_discover_workspace(int(B), int(T), int(max_len)))
+
+
 def discover_fgrams(token_ids: torch.Tensor, max_len: int, S: int, min_count: int = 5,
-                    stream=None):
+                    workspace: Optional[torch.Tensor] = None, stream=None):
     """scone_discover_fgrams: the S most frequent n-grams (2 <= n <= max_len) of
     the [B, T] token matrix.  Returns (fgrams [n, max_len], lengths [n],
-    counts [n]) as CUDA int32 tensors, n = min(S, candidates)."""
+    counts [n]) as CUDA int32 tensors, n = min(S, candidates).  The scratch
+    is `workspace` (a CUDA uint8 tensor of discover_workspace_bytes) or, when
+    None, a tensor from torch's caching allocator, so that repeated calls
+    allocate no device memory."""
     _dev_i32(token_ids, "token_ids", 2)
     B, T = token_ids.shape
     dev = token_ids.device
+    need = discover_workspace_bytes(B, T, max_len)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    if workspace is not None and (workspace.dtype != torch.uint8 or workspace.device != dev
+                                  or not workspace.is_contiguous()):
+        raise ValueError("workspace must be a contiguous uint8 tensor on the tokens' device")
     fg = torch.empty((max(S, 1), max_len), dtype=torch.int32, device=dev)
     ln = torch.empty(max(S, 1), dtype=torch.int32, device=dev)
     ct = torch.empty(max(S, 1), dtype=torch.int32, device=dev)
@@ -232,6 +248,8 @@ def discover_fgrams(token_ids: torch.Tensor, max_len: int, S: int, min_count: in
     with torch.cuda.device(dev):
         rc = lib().scone_discover_fgrams(_ptr(token_ids), B, T, int(max_len), int(min_count),
                                          int(S), _ptr(fg), _ptr(ln), _ptr(ct), ctypes.byref(n),
+                                         _ptr(workspace),
+                                         0 if workspace is None else workspace.numel(),
                                          _stream(stream))
     _check(rc, "scone_discover_fgrams")
     k = n.value

@@ -62,12 +62,14 @@ def test_host_side_argument_errors():
     # discovery: corpora whose candidates a 32-bit counter cannot count
     n = ctypes.c_int64(-1)
     assert L.scone_discover_fgrams(None, 1, 1 << 31, 3, 5, 10, None, None, None,
-                                   ctypes.byref(n), None) == E          # B * T >= 2^31
+                                   ctypes.byref(n), None, 0, None) == E          # B * T >= 2^31
     assert L.scone_discover_fgrams(None, 1, (1 << 31) - 1, 7, 5, 10, None, None, None,
-                                   ctypes.byref(n), None) == E          # 6 * B * T >= 2^32
+                                   ctypes.byref(n), None, 0, None) == E          # 6 * B * T >= 2^32
     assert L.scone_discover_fgrams(None, 1, 1 << 30, 5, 5, 10, None, None, None,
-                                   ctypes.byref(n), None) == E          # 4 * B * T = 2^32
+                                   ctypes.byref(n), None, 0, None) == E          # 4 * B * T = 2^32
     assert n.value == 0
+    assert L.scone_discover_workspace(1, 1 << 30, 5) == -1
+    assert L.scone_discover_workspace(1, 1 << 20, 5) > 2 * (1 << 20) * 16
     # host memory and table bookkeeping
     assert L.scone_host_alloc(0, ctypes.byref(h), ctypes.byref(h)) == E
     assert L.scone_host_free(None) == S.scone.OK

@@ -107,3 +107,38 @@ def test_discovery_edges_and_errors():
     with pytest.raises(S.SconeError) as e:
         S.discover_fgrams(dev(np.array([[1, 2, 2]], np.int32)), 3, 10, 0)
     assert e.value.code == S.scone.EINVAL
+
+
+def test_workspace_paths_agree():
+    """The call with no workspace (it allocates its own), with a caller's
+    workspace reused across calls, and through the binding all give the same
+    top-S set; a short or misaligned workspace is an argument error."""
+    import ctypes
+    rng = np.random.default_rng(21)
+    cdf = zipf_cdf(500)
+    X = zipf_tokens(rng, cdf, (8, 700)).astype(np.int32)
+    K, Sn, mc = 4, 300, 2
+    cands = discovery.candidates(X, K, mc)
+    Xd = dev(X)
+    B, T = X.shape
+    L = S.scone.lib()
+    need = S.discover_workspace_bytes(B, T, K)
+    assert need > 0
+    ws = torch.empty(need + 256, dtype=torch.uint8, device="cuda")
+
+    def call(workspace, nbytes):
+        fg = torch.empty((Sn, K), dtype=torch.int32, device="cuda")
+        ln = torch.empty(Sn, dtype=torch.int32, device="cuda")
+        ct = torch.empty(Sn, dtype=torch.int32, device="cuda")
+        n = ctypes.c_int64()
+        rc = L.scone_discover_fgrams(Xd.data_ptr(), B, T, K, mc, Sn, fg.data_ptr(), ln.data_ptr(),
+                                     ct.data_ptr(), ctypes.byref(n), workspace, nbytes, None)
+        return rc, fg[:n.value], ln[:n.value], ct[:n.value]
+
+    results = [call(None, 0), call(ws.data_ptr(), need), call(ws.data_ptr(), need),
+               (S.scone.OK,) + tuple(S.discover_fgrams(Xd, K, Sn, mc))]
+    for rc, fg, ln, ct in results:
+        assert rc == S.scone.OK
+        check_top_s(fg, ln, ct, cands, Sn)
+    assert call(ws.data_ptr(), need - 1)[0] == S.scone.EINVAL
+    assert call(ws.data_ptr() + 16, need)[0] == S.scone.EINVAL
