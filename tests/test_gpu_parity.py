@@ -458,9 +458,11 @@ def test_tag_lengths_and_histogram(name, max_n):
 # ------------------------------------------------------------ HIP graphs --
 
 def test_graph_capture_replays_match_eager():
-    """lookup + gather, the fused kernel and the split gather captured once and
-    replayed several times, with eager work and syncs between replays."""
-    cfg = scaled(CONFIGS["c2_1m"], n_fgrams=20_000, B=4, T=1000, d=256)
+    """lookup + gather, the fused kernel, the split gather and a pipelined step
+    captured once and replayed several times, with eager work and syncs
+    between replays."""
+    # 1 KiB rows: the pipelined step and the gather take their one-wavefront-per-row kernels
+    cfg = scaled(CONFIGS["c2_1m"], n_fgrams=20_000, B=4, T=1000, d=512)
     w = make_workload(cfg)
     tb = build_gpu(w.fgrams, w.lengths, w.ids)
     E = device_rows(cfg)
@@ -472,6 +474,8 @@ def test_graph_capture_replays_match_eager():
     out_a = torch.empty((cfg.B, cfg.T, cfg.d), dtype=E.dtype, device="cuda")
     out_b = torch.empty_like(out_a)
     out_c = torch.empty_like(out_a)
+    out_d = torch.empty_like(out_a)
+    nxt = torch.empty_like(ids)
     near = E[:cfg.V].contiguous()
     far = S.HostRows(cfg.n_fgrams, (cfg.d,), E.dtype)
     try:
@@ -489,15 +493,17 @@ def test_graph_capture_replays_match_eager():
             S.gather(ids, E, out=out_a)
             S.embed(tb, X, cfg.max_n, E, out=out_b)
             S.gather_split(ids, near, far, ws, out=out_c)
+            S.embed_pipelined(tb, X, cfg.max_n, nxt, ids, E, out=out_d)
         for r in range(4):
-            for t in (ids, out_a, out_b, out_c):
+            for t in (ids, nxt, out_a, out_b, out_c, out_d):
                 t.view(torch.uint8).fill_(0xA5)      # eager work between replays
             torch.cuda.synchronize()
             g.replay()
             torch.cuda.synchronize()
             S.check_ok()
             np.testing.assert_array_equal(ids.cpu().numpy(), exp_ids)
-            for t in (out_a, out_b, out_c):
+            np.testing.assert_array_equal(nxt.cpu().numpy(), exp_ids)
+            for t in (out_a, out_b, out_c, out_d):
                 assert as_bytes(t).tobytes() == exp.tobytes(), r
     finally:
         far.close()

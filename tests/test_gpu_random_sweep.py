@@ -5,8 +5,8 @@ query stream itself, so every length hits; half random), a query matrix with
 ragged tails, a window max_n on either side of K and a row table of an odd or
 even width, then checks every call through the C ABI against the CPU oracle:
 lookup ids and lengths, the tagger's lengths and histogram, the gather and the
-fused kernel byte for byte, decoding step by step against prefill, and the
-split placement.  The sweep is deterministic (fixed seeds) and prints the case
+fused kernel byte for byte, a two-batch pipelined stream, decoding step by step
+against prefill, and the split placement.  The sweep is deterministic (fixed seeds) and prints the case
 it is on.
 """
 import numpy as np
@@ -84,6 +84,26 @@ def test_random_sweep(block):
                                       err_msg=what)
         assert as_bytes(out).tobytes() == exp_rows.tobytes(), what
         assert as_bytes(fused).tobytes() == exp_rows.tobytes(), what
+
+        # pipelined step, a stream of two batches (X, then X reversed along T):
+        # step 0 looks up X; step 1 looks up the second batch while gathering
+        # X's rows, on the case's row width (one launch for 1/2/4/8 KiB rows,
+        # the two kernels otherwise) and on a random width of whole KiB
+        X2 = np.ascontiguousarray(X[:, ::-1])
+        exp_ids2, _ = o.lookup(X2, max_n)
+        rng2 = np.random.default_rng(19000 + case)
+        rb2 = int(rng2.choice([1024, 2048, 4096, 8192]))
+        table2 = rng2.integers(0, 256, size=(n_rows, rb2), dtype=np.uint8)
+        for tab, Et, exp_r in ((table, E, exp_rows),
+                               (table2, dev(table2), oracle.gather(exp_ids, table2))):
+            p0 = torch.empty((B, T), dtype=torch.int32, device="cuda")
+            p1 = torch.empty((B, T), dtype=torch.int32, device="cuda")
+            S.embed_pipelined(tb, Xd, max_n, p0, None, Et)
+            pout = S.embed_pipelined(tb, dev(X2), max_n, p1, p0, Et)
+            S.check_ok()
+            np.testing.assert_array_equal(p0.cpu().numpy(), exp_ids, err_msg=what)
+            np.testing.assert_array_equal(p1.cpu().numpy(), exp_ids2, err_msg=what)
+            assert as_bytes(pout).tobytes() == exp_r.tobytes(), what
 
         if row_bytes % 16 == 0 and B * T > 0:
             # split placement: token rows in HBM, f-gram rows in pinned host memory
