@@ -901,19 +901,21 @@ def run_precompute(args, cfg):
                            "traffic": None,
                            "kernel": "scone_fgram_model_forward (all kernels of one call)",
                            "algorithmic_flops_per_launch": flops}}
-    # parity on a sample of rows, bar of the GPU parity tests (3 eps(L) per row)
-    from oracle import fgram_model as orc
-    rng = np.random.default_rng(0)
-    sample = rng.choice(n, 32, replace=False)
-    T64 = E[:cfg.V].float().cpu().numpy().astype(np.float64)
-    P64 = {k: bf16_bits_to_f64(v) for k, v in P.items()}
-    ref = orc.forward(fg_np[sample], w.lengths[sample], T64, P64, mc.n_layers, mc.n_heads)
-    got = E[torch.from_numpy(w.ids[sample].astype(np.int64)).to(dev)].float().cpu().numpy()
-    rel = np.linalg.norm(got - ref, axis=1) / np.linalg.norm(ref, axis=1)
-    bar = 3 * 2.0 ** -9 * np.sqrt((5 * mc.n_layers + 2) / 3)
-    result["parity"] = {"sample_rows": len(sample), "max_row_rel_err": float(rel.max()),
-                        "bar": bar, "ok": bool(rel.max() <= bar)}
+    result["cpu_baseline"] = None
     if not args.no_cpu_baseline:
+        # The CPU-baseline leg: parity of a sample of rows with the oracle (the
+        # bar of the GPU parity tests, 3 eps(L) per row), then the oracle timed.
+        from oracle import fgram_model as orc
+        rng = np.random.default_rng(0)
+        sample = rng.choice(n, 32, replace=False)
+        T64 = E[:cfg.V].float().cpu().numpy().astype(np.float64)
+        P64 = {k: bf16_bits_to_f64(v) for k, v in P.items()}
+        ref = orc.forward(fg_np[sample], w.lengths[sample], T64, P64, mc.n_layers, mc.n_heads)
+        got = E[torch.from_numpy(w.ids[sample].astype(np.int64)).to(dev)].float().cpu().numpy()
+        rel = np.linalg.norm(got - ref, axis=1) / np.linalg.norm(ref, axis=1)
+        bar = 3 * 2.0 ** -9 * np.sqrt((5 * mc.n_layers + 2) / 3)
+        result["parity"] = {"sample_rows": len(sample), "max_row_rel_err": float(rel.max()),
+                            "bar": bar, "ok": bool(rel.max() <= bar)}
         cs = rng.choice(n, 64, replace=False)
         t0 = time.perf_counter()
         reps = 0
