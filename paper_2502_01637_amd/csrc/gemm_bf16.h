@@ -43,6 +43,16 @@ enum Epilogue { kBias = 0, kGelu = 1, kResid = 2 };
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
 
+// Two floats to two bf16 in one word (a low, b high), rounded to nearest,
+// ties to even, by the hardware conversion (v_cvt_pk_bf16_f32): the same
+// bits as f32_to_bf16 below for every finite float (checked on gfx950 over
+// all 2^32 bit patterns), in one instruction instead of about eight.
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2{a, b}), bf16x2));
+}
+
 // Round to nearest, ties to even (inputs are finite).
 __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
     const uint32_t u = __float_as_uint(f);
@@ -251,8 +261,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
                     v0 = gelu_erf(v0); v1 = gelu_erf(v1); v2 = gelu_erf(v2); v3 = gelu_erf(v3);
                 }
                 u32x2 o;
-                o.x = f32_to_bf16(v0) | (f32_to_bf16(v1) << 16);
-                o.y = f32_to_bf16(v2) | (f32_to_bf16(v3) << 16);
+                o.x = pack_bf16x2(v0, v1);
+                o.y = pack_bf16x2(v2, v3);
                 *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(out) + (int64_t)m * ldc + n) = o;
             }
         }
