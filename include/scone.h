@@ -73,13 +73,20 @@ enum scone_placement {
  *           ignored and may hold anything).
  *  lengths  [n] int32, each in [2, max_len]   (else SCONE_ELEN; V_fgram is a
  *           subset of V^[2,K]).
- *  ids      [n] int32 row ids, each >= 0      (else SCONE_EID).  Ids are not
- *           checked against a row count here; scone_gather checks them.
+ *  ids      [n] int32 row ids, each in [0, 2^31 - 1)   (else SCONE_EID; the
+ *           value 2^31 - 1 is reserved).  Ids are not checked against a row
+ *           count here; scone_gather checks them.
  *  n        number of f-grams, >= 0 (0 builds an empty set).
  *  max_len  K, in [2, SCONE_MAX_FGRAM_LEN].  K <= 5 uses 16-byte slots,
  *           K = 6 or 7 uses 32-byte slots.
  *  max_load target load factor in (0, 0.9]; the slot count is the smallest
- *           power of two >= max(64, n / max_load).
+ *           power of two >= max(64, e / max_load), where e is n plus the
+ *           number of f-grams of length >= 4 plus the number of length >= 6.
+ *           Besides the f-grams, the table holds an entry for the last three
+ *           tokens of every f-gram of length >= 4 and the last five of every
+ *           f-gram of length >= 6, flagged so that a lookup stops probing a
+ *           position once no longer f-gram can end there; e bounds all of
+ *           them.
  *  stream   stream on which the inputs are ready.
  *  out      receives the new table handle (host pointer to a handle).
  *

@@ -69,7 +69,7 @@ __global__ __launch_bounds__(kTileThreads) void k_embed(
         int32_t id;
         int len;
         bool tok_ok;
-        tile_lookup<SB, G>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok);
+        tile_lookup<SB, G, false>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok);
         const int p = threadIdx.x / G;
         const int64_t t = t0 + p;
         if (threadIdx.x % G == 0 && p < P) {

@@ -28,8 +28,9 @@ __global__ __launch_bounds__(kTileThreads) void k_pipelined(
     __shared__ int32_t s_tok[TileShape<G>::kPositions + kMaxHalo];
     const int64_t blk = block_index(block0);
     if (blk < n_lookup_blocks) {  // workgroup-uniform
-        lookup_block<SB, G>(slots, mask, X, T, max_n, tiles_per_row, blk, s_tok, next_ids,
-                            next_len, err);
+        // pruned probes: fewer bucket lines compete with the row stream
+        lookup_block<SB, G, (G >= 4)>(slots, mask, X, T, max_n, tiles_per_row, blk, s_tok,
+                                      next_ids, next_len, err);
         return;
     }
     const int64_t r = (blk - n_lookup_blocks) * (kTileThreads / 64) +

@@ -177,10 +177,27 @@ __device__ __forceinline__ uint64_t home_slot(const Key& k, uint64_t mask, int b
     return (hash_key(k) & mask) & ~(uint64_t)(bucket_slots - 1);
 }
 
-// Returns true and the id on a hit.  Bounded by the slot count.
+// The id word of a slot.  Bits 0..30 hold the f-gram's row id, or
+// kMarkerId for a marker: an entry that is not an f-gram but the suffix of
+// one (see kExtBit).  Bit 31, kExtBit, is set on the entry of a length-3 key
+// when some f-gram of length 4 or more ends with those three tokens, and on
+// the entry of a length-5 key when some f-gram of length 6 or more ends with
+// those five; every such suffix has an entry (the f-gram itself or a marker).
+// A lookup can therefore skip the probes of lengths 4-5 (6-7) at a position
+// whose length-3 (length-5) suffix has no entry with the bit, and the result
+// is the same as probing every length.
+constexpr uint32_t kExtBit = 0x80000000u;
+constexpr int32_t kIdMask = 0x7FFFFFFF;
+constexpr int32_t kMarkerId = 0x7FFFFFFF;  // a row id the build rejects
+
+__device__ __forceinline__ bool entry_is_fgram(int32_t raw) { return (raw & kIdMask) != kMarkerId; }
+__device__ __forceinline__ bool entry_extends(int32_t raw) { return raw < 0; }
+
+// Returns true and the slot's raw id word when the key has an entry (an
+// f-gram or a marker).  Bounded by the slot count.
 template <int SB>
-__device__ __forceinline__ bool probe(const typename SlotOps<SB>::Slot* slots, uint64_t mask,
-                                      const Key& k, int32_t& id_out) {
+__device__ __forceinline__ bool probe_raw(const typename SlotOps<SB>::Slot* slots, uint64_t mask,
+                                          const Key& k, int32_t& raw_out) {
     constexpr int BW = Bucket<SB>::kSlots;
     uint64_t s = home_slot(k, mask, BW);
     for (uint64_t step = 0; step <= mask; step += BW) {
@@ -192,7 +209,7 @@ __device__ __forceinline__ bool probe(const typename SlotOps<SB>::Slot* slots, u
 #pragma unroll
         for (int i = 0; i < BW; ++i) {
             if (w0[i] == k.w0 && w1[i] == k.w1) {
-                id_out = id[i];
+                raw_out = id[i];
                 return true;
             }
             empty |= w0[i] == 0;
@@ -203,6 +220,16 @@ __device__ __forceinline__ bool probe(const typename SlotOps<SB>::Slot* slots, u
     return false;
 }
 
+// Returns true and the row id when the key is an f-gram of the table.
+template <int SB>
+__device__ __forceinline__ bool probe(const typename SlotOps<SB>::Slot* slots, uint64_t mask,
+                                      const Key& k, int32_t& id_out) {
+    int32_t raw = 0;
+    if (!probe_raw<SB>(slots, mask, k, raw) || !entry_is_fgram(raw)) return false;
+    id_out = raw & kIdMask;
+    return true;
+}
+
 }  // namespace scone
 
 struct scone_table;
@@ -210,10 +237,11 @@ struct scone_table;
 namespace scone {
 // Launch the lookup kernel (max_n already clamped to the table's K); a null
 // `ids`, `lens` or `hist` output is skipped.  `hist` accumulates, per matched
-// length 1..K, the number of positions (index = length).
+// length 1..K, the number of positions (index = length).  `prune` selects
+// the probe schedule of tile_lookup (same results either way).
 hipError_t launch_lookup(const scone_table* tb, const int32_t* X, int64_t B, int64_t T,
                          int max_n, int32_t* ids, int8_t* lens, unsigned* err, hipStream_t st,
-                         unsigned long long* hist = nullptr);
+                         unsigned long long* hist = nullptr, bool prune = false);
 // Zero `bytes` of device memory with a kernel and raise SCONE_EROW (a table
 // without rows has no valid row id).
 hipError_t launch_zero_rows(void* out, int64_t bytes, unsigned* err, hipStream_t st);

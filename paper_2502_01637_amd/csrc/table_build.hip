@@ -10,6 +10,15 @@
 // placement under concurrency does not matter.  A second pass re-probes every
 // input key: the first slot holding that key must be the one its own thread
 // claimed, otherwise the key was inserted twice (a duplicate f-gram).
+//
+// A third pass adds the suffix entries that let lookups skip probes: for
+// every f-gram of length 4 or more, the entry of its last three tokens gets
+// kExtBit, and for every f-gram of length 6 or more, so does the entry of its
+// last five; where that suffix is not itself an f-gram, a marker entry
+// (id kMarkerId) is inserted for it.  Two threads may insert the same marker
+// at once, leaving two identical copies; lookups read whichever comes first
+// on the probe path, so that costs a slot and nothing else.  The slot count
+// allows for one marker per such suffix.
 #include <algorithm>
 #include <cmath>
 
@@ -42,7 +51,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_insert(
         atomicOr(status, err_bit(SCONE_ELEN));
         return;
     }
-    if (id < 0) {
+    if (id < 0 || id == kMarkerId) {
         atomicOr(status, err_bit(SCONE_EID));
         return;
     }
@@ -91,6 +100,79 @@ __global__ __launch_bounds__(kBuildThreads) void k_verify(
     atomicOr(status, err_bit(SCONE_EFULL));
 }
 
+// Counts the f-grams of length 4..max_len and 6..max_len (the suffix
+// entries the third pass may add).
+__global__ __launch_bounds__(kBuildThreads) void k_count_long(
+    const int32_t* __restrict__ lengths, int64_t n, int max_len,
+    unsigned long long* __restrict__ counts, int64_t block0) {
+    const int64_t k = block_index(block0) * kBuildThreads + threadIdx.x;
+    const int len = k < n ? lengths[k] : 0;
+    const unsigned long long c4 = __popcll(__ballot(len >= 4 && len <= max_len));
+    const unsigned long long c6 = __popcll(__ballot(len >= 6 && len <= max_len));
+    if ((threadIdx.x & 63) == 0) {
+        if (c4) atomicAdd(counts, c4);
+        if (c6) atomicAdd(counts + 1, c6);
+    }
+}
+
+// Gives the entry of `key` kExtBit, inserting a marker when the key has no
+// entry.  A marker slot is claimed in three steps: its first key word goes
+// from 0 to kBusy (no key has length field 15), the rest of the key and the
+// id are written, and only then is the first word set to the key with
+// release order.  A thread that reads the first word with acquire order and
+// finds a key therefore also sees that key's second word, so it never takes
+// a half-written slot for its own key; a slot still kBusy counts as another
+// key (at worst a second, identical marker).
+constexpr uint64_t kBusy = 0xF;
+
+template <int SB>
+__device__ __forceinline__ void mark_suffix(typename SlotOps<SB>::Slot* slots, uint64_t mask,
+                                            const Key& key, unsigned* status) {
+    uint64_t s = home_slot(key, mask, Bucket<SB>::kSlots);
+    for (uint64_t step = 0; step <= mask; ++step) {
+        unsigned long long* w0p = reinterpret_cast<unsigned long long*>(&slots[s].w0);
+        uint64_t w0 = __hip_atomic_load(w0p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+        if (w0 == 0) {
+            w0 = atomicCAS(w0p, 0ull, (unsigned long long)kBusy);
+            if (w0 == 0) {
+                SlotOps<SB>::write_rest(slots, s, key, (int32_t)(kMarkerId | kExtBit));
+                __hip_atomic_store(w0p, (unsigned long long)key.w0, __ATOMIC_RELEASE,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+                return;
+            }
+            w0 = __hip_atomic_load(w0p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        if (w0 == key.w0) {
+            uint64_t w1;
+            if (SB == 16)
+                w1 = __hip_atomic_load(reinterpret_cast<uint32_t*>(&slots[s]) + 2,
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            else
+                w1 = __hip_atomic_load(reinterpret_cast<unsigned long long*>(&slots[s]) + 1,
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (w1 == key.w1) {
+                atomicOr(reinterpret_cast<unsigned*>(&slots[s].id), kExtBit);
+                return;
+            }
+        }
+        s = (s + 1) & mask;
+    }
+    atomicOr(status, err_bit(SCONE_EFULL));
+}
+
+template <int SB>
+__global__ __launch_bounds__(kBuildThreads) void k_mark(
+    const int32_t* __restrict__ fgrams, const int32_t* __restrict__ lengths, int64_t n,
+    int max_len, typename SlotOps<SB>::Slot* __restrict__ slots, uint64_t mask,
+    const int64_t* __restrict__ slot_of, unsigned* __restrict__ status, int64_t block0) {
+    const int64_t k = block_index(block0) * kBuildThreads + threadIdx.x;
+    if (k >= n || slot_of[k] < 0) return;  // rejected f-grams were reported
+    const int len = lengths[k];
+    const int32_t* tok = fgrams + k * (int64_t)max_len;
+    if (len >= 4) mark_suffix<SB>(slots, mask, pack_key(tok + len - 3, 3), status);
+    if (len >= 6) mark_suffix<SB>(slots, mask, pack_key(tok + len - 5, 5), status);
+}
+
 template <int SB>
 hipError_t launch_build(const int32_t* fgrams, const int32_t* lengths, const int32_t* ids,
                         int64_t n, int max_len, void* slots, uint64_t mask, int64_t* slot_of,
@@ -102,9 +184,14 @@ hipError_t launch_build(const int32_t* fgrams, const int32_t* lengths, const int
                            n, max_len, static_cast<Slot*>(slots), mask, slot_of, status, b0);
     });
     if (e != hipSuccess) return e;
-    return launch_blocks(blocks, kBuildThreads, [&](int64_t b0, dim3 grid) {
+    const hipError_t e2 = launch_blocks(blocks, kBuildThreads, [&](int64_t b0, dim3 grid) {
         hipLaunchKernelGGL(k_verify<SB>, grid, dim3(kBuildThreads), 0, st, fgrams, lengths, n,
                            max_len, static_cast<const Slot*>(slots), mask, slot_of, status, b0);
+    });
+    if (e2 != hipSuccess || max_len < 4) return e2;
+    return launch_blocks(blocks, kBuildThreads, [&](int64_t b0, dim3 grid) {
+        hipLaunchKernelGGL(k_mark<SB>, grid, dim3(kBuildThreads), 0, st, fgrams, lengths, n,
+                           max_len, static_cast<Slot*>(slots), mask, slot_of, status, b0);
     });
 }
 
@@ -120,11 +207,9 @@ extern "C" int scone_build_fgram_table(const int32_t* fgrams, const int32_t* len
     if (n < 0 || max_len < 2 || max_len > SCONE_MAX_FGRAM_LEN) return SCONE_EINVAL;
     if (!(max_load > 0.0 && max_load <= 0.9)) return SCONE_EINVAL;
     if (n > 0 && (!fgrams || !lengths || !ids)) return SCONE_EINVAL;
-    // Slot count: smallest power of two >= max(64, n / max_load), at most 2^40.
-    const double want = std::max(64.0, std::ceil((double)n / max_load));
-    if (want > (double)(1ull << 40)) return SCONE_EINVAL;
-    uint64_t cap = 64;
-    while ((double)cap < want) cap <<= 1;
+    // At most n entries plus one suffix entry per f-gram of length >= 4 and
+    // one more per f-gram of length >= 6, so n * 3 bounds them.
+    if (std::ceil(3.0 * (double)n / max_load) > (double)(1ull << 40)) return SCONE_EINVAL;
     const int slot_bytes = max_len <= kMaxLenSlot16 ? 16 : 32;
 
     hipStream_t st = static_cast<hipStream_t>(stream);
@@ -132,22 +217,52 @@ extern "C" int scone_build_fgram_table(const int32_t* fgrams, const int32_t* len
     SCONE_HIP_TRY(hipGetDevice(&dev));
 
     void* slots = nullptr;
-    unsigned* status = nullptr;
+    // status word at offset 0, counts of f-grams of length >= 4 and >= 6 at 8, 16
+    void* aux = nullptr;
     int64_t* slot_of = nullptr;
     int rc = SCONE_OK;
     unsigned hstatus = 0;
-    if (hipMalloc(&slots, cap * (uint64_t)slot_bytes) != hipSuccess) {
+    unsigned long long hcount[2] = {0, 0};
+    uint64_t cap = 64;
+    unsigned* status = nullptr;
+    if (hipMalloc(&aux, 32) != hipSuccess) {
         (void)hipGetLastError();
         return SCONE_ENOMEM;
     }
-    if (hipMalloc(&status, sizeof(unsigned)) != hipSuccess ||
+    status = static_cast<unsigned*>(aux);
+    if (hipMemsetAsync(aux, 0, 32, st) != hipSuccess) {
+        rc = SCONE_EHIP;
+        goto fail;
+    }
+    if (n > 0 && max_len >= 4) {
+        unsigned long long* counts =
+            reinterpret_cast<unsigned long long*>(static_cast<uint8_t*>(aux) + 8);
+        const hipError_t e = launch_blocks((n + kBuildThreads - 1) / kBuildThreads, kBuildThreads,
+                                           [&](int64_t b0, dim3 grid) {
+            hipLaunchKernelGGL(k_count_long, grid, dim3(kBuildThreads), 0, st, lengths, n,
+                               (int)max_len, counts, b0);
+        });
+        if (e != hipSuccess ||
+            hipMemcpyAsync(hcount, counts, sizeof(hcount), hipMemcpyDeviceToHost, st) !=
+                hipSuccess ||
+            hipStreamSynchronize(st) != hipSuccess) {
+            rc = SCONE_EHIP;
+            goto fail;
+        }
+    }
+    {
+        // Slot count: smallest power of two >= max(64, entries / max_load).
+        const double entries = (double)n + (double)hcount[0] + (double)hcount[1];
+        const double want = std::max(64.0, std::ceil(entries / max_load));
+        while ((double)cap < want) cap <<= 1;
+    }
+    if (hipMalloc(&slots, cap * (uint64_t)slot_bytes) != hipSuccess ||
         (n > 0 && hipMalloc(&slot_of, sizeof(int64_t) * (size_t)n) != hipSuccess)) {
         (void)hipGetLastError();
         rc = SCONE_ENOMEM;
         goto fail;
     }
-    if (hipMemsetAsync(slots, 0, cap * (uint64_t)slot_bytes, st) != hipSuccess ||
-        hipMemsetAsync(status, 0, sizeof(unsigned), st) != hipSuccess) {
+    if (hipMemsetAsync(slots, 0, cap * (uint64_t)slot_bytes, st) != hipSuccess) {
         rc = SCONE_EHIP;
         goto fail;
     }
@@ -180,7 +295,7 @@ extern "C" int scone_build_fgram_table(const int32_t* fgrams, const int32_t* len
             }
         goto fail;
     }
-    (void)hipFree(status);
+    (void)hipFree(aux);
     if (slot_of) (void)hipFree(slot_of);
     {
         scone_table* t = new (std::nothrow) scone_table();
@@ -201,7 +316,7 @@ extern "C" int scone_build_fgram_table(const int32_t* fgrams, const int32_t* len
 fail:
     (void)hipStreamSynchronize(st);
     if (slots) (void)hipFree(slots);
-    if (status) (void)hipFree(status);
+    if (aux) (void)hipFree(aux);
     if (slot_of) (void)hipFree(slot_of);
     return rc;
 }

@@ -30,12 +30,21 @@ __device__ __forceinline__ void stage_tokens(int32_t* s_tok, const int32_t* __re
 
 // After stage_tokens and a barrier: position p = threadIdx.x / G (p < P) of
 // the tile gets its longest match.  Lane j of the position's group probes the
-// suffix of length max_n - j; a wave ballot picks the lowest hitting lane (the
-// longest match) and a shuffle brings its id to lane j = 0.  Returns, on lane
-// j = 0 of a valid position (p < P, t0 + p < T), the id (or the token itself)
-// and the matched length (1 when nothing matched); `tok_ok` reports whether
-// the position's own token is in range.  All lanes of the wave must call it.
-template <int SB, int G>
+// suffix of length max_n - j.  Without kPrune every length is probed at once.
+// With kPrune, lengths 2 and 3 are probed first; lengths 4 and 5 only when
+// the length-3 suffix has an entry with kExtBit (some f-gram of length >= 4
+// ends with it), and lengths 6 and 7 only when the length-5 suffix does too,
+// so a position stops as soon as no longer f-gram can end there (on a
+// workload of 10M f-grams of length 2..5, 2.75 probes per position instead
+// of 4).  Pruning saves memory traffic but adds dependent rounds, so it pays
+// where many lookups share the memory system (a lookup overlapped with a row
+// stream, a corpus-sized tagging pass) and costs latency where one small
+// lookup runs alone.  A wave ballot then picks the lowest hitting lane (the
+// longest match) and a shuffle brings its id to lane j = 0.  Returns, on lane j = 0 of a valid
+// position (p < P, t0 + p < T), the id (or the token itself) and the matched
+// length (1 when nothing matched); `tok_ok` reports whether the position's
+// own token is in range.  All lanes of the wave must call it.
+template <int SB, int G, bool kPrune>
 __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __restrict__ slots,
                                             uint64_t mask, const int32_t* s_tok, int64_t T,
                                             int64_t t0, int P, int max_n, int32_t& id_out,
@@ -46,20 +55,37 @@ __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __
     const int64_t t = t0 + p;
     const bool valid = p < P && t < T;
     const int n = max_n - j;
-    bool hit = false;
+    const bool can = valid && n >= 2 && (int64_t)n <= t + 1;
+    const int lane = threadIdx.x & 63;
+    const int base = lane & ~(G - 1);
+    const unsigned group = (1u << G) - 1u;
+    bool hit = false, ext = false;
     int32_t id = 0;
-    if (valid && n >= 2 && (int64_t)n <= t + 1) {
+    auto probe_here = [&](bool active) {
+        if (!active) return;
         const int32_t* win = s_tok + p + halo - n + 1;  // X[b, t-n+1 .. t]
         bool ok = true;
 #pragma unroll
         for (int i = 0; i < SCONE_MAX_FGRAM_LEN; ++i)
             if (i < n) ok &= (win[i] >= 0) & (win[i] < SCONE_TOKEN_LIMIT);
-        if (ok) hit = probe<SB>(slots, mask, pack_key(win, n), id);
+        int32_t raw = 0;
+        if (ok && probe_raw<SB>(slots, mask, pack_key(win, n), raw)) {
+            hit = entry_is_fgram(raw);
+            id = raw & kIdMask;
+            ext = entry_extends(raw);
+        }
+    };
+    probe_here(can && (n <= 3 || !kPrune));
+    if (kPrune && max_n >= 4) {  // the same for every lane of the launch
+        const bool go4 = ((unsigned)(__ballot(ext && n == 3) >> base) & group) != 0;
+        probe_here(can && go4 && n >= 4 && n <= 5);
+        if (max_n >= 6) {
+            const bool go6 = ((unsigned)(__ballot(ext && n == 5) >> base) & group) != 0;
+            probe_here(can && go6 && n >= 6);
+        }
     }
     const unsigned long long m = __ballot(hit);
-    const int lane = threadIdx.x & 63;
-    const int base = lane & ~(G - 1);
-    const unsigned gm = (unsigned)(m >> base) & ((1u << G) - 1u);
+    const unsigned gm = (unsigned)(m >> base) & group;
     const int jb = gm ? __ffs(gm) - 1 : 0;
     const int32_t best = __shfl(id, base + jb);
     const int32_t tok = valid ? s_tok[p + halo] : 0;
@@ -74,7 +100,7 @@ __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __
 // length (either output may be null); a bad token raises SCONE_ETOKEN.
 // Returns the matched length on the lane that wrote a position, else 0.
 // Called by the whole workgroup (it synchronises once).
-template <int SB, int G>
+template <int SB, int G, bool kPrune>
 __device__ __forceinline__ int lookup_block(const typename SlotOps<SB>::Slot* __restrict__ slots,
                                             uint64_t mask, const int32_t* __restrict__ X,
                                             int64_t T, int max_n, int64_t tiles_per_row,
@@ -90,7 +116,7 @@ __device__ __forceinline__ int lookup_block(const typename SlotOps<SB>::Slot* __
     int32_t id;
     int len;
     bool tok_ok;
-    tile_lookup<SB, G>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok);
+    tile_lookup<SB, G, kPrune>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok);
     const int64_t t = t0 + threadIdx.x / G;
     if (threadIdx.x % G == 0 && t < T) {
         if (!tok_ok) atomicOr(err, err_bit(SCONE_ETOKEN));
