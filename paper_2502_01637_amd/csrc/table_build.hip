@@ -105,24 +105,31 @@ __global__ __launch_bounds__(kBuildThreads) void k_verify(
 __global__ __launch_bounds__(kBuildThreads) void k_count_long(
     const int32_t* __restrict__ lengths, int64_t n, int max_len,
     unsigned long long* __restrict__ counts, int64_t block0) {
+    __shared__ unsigned s_c[2];
+    if (threadIdx.x < 2) s_c[threadIdx.x] = 0;
+    __syncthreads();
     const int64_t k = block_index(block0) * kBuildThreads + threadIdx.x;
     const int len = k < n ? lengths[k] : 0;
-    const unsigned long long c4 = __popcll(__ballot(len >= 4 && len <= max_len));
-    const unsigned long long c6 = __popcll(__ballot(len >= 6 && len <= max_len));
+    const unsigned c4 = (unsigned)__popcll(__ballot(len >= 4 && len <= max_len));
+    const unsigned c6 = (unsigned)__popcll(__ballot(len >= 6 && len <= max_len));
     if ((threadIdx.x & 63) == 0) {
-        if (c4) atomicAdd(counts, c4);
-        if (c6) atomicAdd(counts + 1, c6);
+        if (c4) atomicAdd(&s_c[0], c4);
+        if (c6) atomicAdd(&s_c[1], c6);
     }
+    __syncthreads();
+    // one global add per workgroup and counter (same-address atomics serialise)
+    if (threadIdx.x < 2 && s_c[threadIdx.x])
+        atomicAdd(counts + threadIdx.x, (unsigned long long)s_c[threadIdx.x]);
 }
 
 // Gives the entry of `key` kExtBit, inserting a marker when the key has no
 // entry.  A marker slot is claimed in three steps: its first key word goes
 // from 0 to kBusy (no key has length field 15), the rest of the key and the
 // id are written, and only then is the first word set to the key with
-// release order.  A thread that reads the first word with acquire order and
-// finds a key therefore also sees that key's second word, so it never takes
-// a half-written slot for its own key; a slot still kBusy counts as another
-// key (at worst a second, identical marker).
+// release order.  A thread that reads its key in the first word and then
+// takes an acquire fence therefore also sees that key's second word, so it
+// never takes a half-written slot for its own key; a slot still kBusy counts
+// as another key (at worst a second, identical marker).
 constexpr uint64_t kBusy = 0xF;
 
 template <int SB>
@@ -131,7 +138,7 @@ __device__ __forceinline__ void mark_suffix(typename SlotOps<SB>::Slot* slots, u
     uint64_t s = home_slot(key, mask, Bucket<SB>::kSlots);
     for (uint64_t step = 0; step <= mask; ++step) {
         unsigned long long* w0p = reinterpret_cast<unsigned long long*>(&slots[s].w0);
-        uint64_t w0 = __hip_atomic_load(w0p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+        uint64_t w0 = __hip_atomic_load(w0p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (w0 == 0) {
             w0 = atomicCAS(w0p, 0ull, (unsigned long long)kBusy);
             if (w0 == 0) {
@@ -140,9 +147,12 @@ __device__ __forceinline__ void mark_suffix(typename SlotOps<SB>::Slot* slots, u
                                    __HIP_MEMORY_SCOPE_AGENT);
                 return;
             }
-            w0 = __hip_atomic_load(w0p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+            w0 = __hip_atomic_load(w0p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         if (w0 == key.w0) {
+            // the release store that published this key word happened before:
+            // an acquire fence makes the rest of the slot visible
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
             uint64_t w1;
             if (SB == 16)
                 w1 = __hip_atomic_load(reinterpret_cast<uint32_t*>(&slots[s]) + 2,
@@ -151,7 +161,11 @@ __device__ __forceinline__ void mark_suffix(typename SlotOps<SB>::Slot* slots, u
                 w1 = __hip_atomic_load(reinterpret_cast<unsigned long long*>(&slots[s]) + 1,
                                        __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (w1 == key.w1) {
-                atomicOr(reinterpret_cast<unsigned*>(&slots[s].id), kExtBit);
+                // common suffixes end many f-grams: skip the atomic once the bit is set
+                unsigned* idp = reinterpret_cast<unsigned*>(&slots[s].id);
+                if (!(__hip_atomic_load(idp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
+                      kExtBit))
+                    atomicOr(idp, kExtBit);
                 return;
             }
         }
