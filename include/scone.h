@@ -46,7 +46,7 @@ enum scone_status {
     SCONE_OK = 0,
     SCONE_EINVAL = 1,  /* bad argument: null pointer, negative size, bad window ... */
     SCONE_ELEN = 2,    /* an f-gram length outside [2, max_len] */
-    SCONE_EID = 3,     /* a negative f-gram id */
+    SCONE_EID = 3,     /* an f-gram id outside [0, 2^31 - 1) */
     SCONE_EDUP = 4,    /* the same f-gram appears twice in the build input */
     SCONE_EFULL = 5,   /* hash table has no free slot (cannot happen for max_load <= 0.9) */
     SCONE_ENOMEM = 6,  /* device or pinned host allocation failed */

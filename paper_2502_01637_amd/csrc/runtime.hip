@@ -64,7 +64,7 @@ const char* scone_strerror(int code) {
         case SCONE_OK: return "ok";
         case SCONE_EINVAL: return "invalid argument";
         case SCONE_ELEN: return "f-gram length outside [2, max_len]";
-        case SCONE_EID: return "negative f-gram id";
+        case SCONE_EID: return "f-gram id outside [0, 2^31 - 1)";
         case SCONE_EDUP: return "duplicate f-gram in build input";
         case SCONE_EFULL: return "hash table full";
         case SCONE_ENOMEM: return "out of memory";
