@@ -938,7 +938,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default=DEFAULT_CONFIG)
-    ap.add_argument("--max-load", type=float, default=0.5)
+    ap.add_argument("--max-load", type=float, default=0.25,
+                    help="hash-table load target (slots >= entries / max_load)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--tag", action="store_true",

@@ -158,7 +158,7 @@ class Table:
 
 
 def build_fgram_table(fgrams: torch.Tensor, lengths: torch.Tensor, ids: torch.Tensor,
-                      max_load: float = 0.5, stream=None) -> Table:
+                      max_load: float = 0.25, stream=None) -> Table:
     """scone_build_fgram_table: fgrams [n, K] int32, lengths [n], ids [n] (device)."""
     _dev_i32(fgrams, "fgrams", 2)
     _dev_i32(lengths, "lengths", 1)
