@@ -69,7 +69,7 @@ __global__ __launch_bounds__(kTileThreads) void k_embed(
         int32_t id;
         int len;
         bool tok_ok;
-        tile_lookup<SB, G, false>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok);
+        tile_lookup<SB, G>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok);
         const int p = threadIdx.x / G;
         const int64_t t = t0 + p;
         if (threadIdx.x % G == 0 && p < P) {
@@ -147,20 +147,11 @@ template <int SB, typename V, bool kPow2>
 hipError_t dispatch(const scone_table* tb, const int32_t* X, int64_t B, int64_t T, int max_n,
                     const void* rows, int64_t n_rows, int64_t upr, int shift, void* out,
                     int32_t* ids, int8_t* lens, unsigned* err, hipStream_t st) {
-    switch (lanes_for(max_n)) {
-        case 1:
-            return launch<SB, 1, V, kPow2>(tb, X, B, T, max_n, rows, n_rows, upr, shift, out,
-                                           ids, lens, err, st);
-        case 2:
-            return launch<SB, 2, V, kPow2>(tb, X, B, T, max_n, rows, n_rows, upr, shift, out,
-                                           ids, lens, err, st);
-        case 4:
-            return launch<SB, 4, V, kPow2>(tb, X, B, T, max_n, rows, n_rows, upr, shift, out,
-                                           ids, lens, err, st);
-        default:
-            return launch<SB, 8, V, kPow2>(tb, X, B, T, max_n, rows, n_rows, upr, shift, out,
-                                           ids, lens, err, st);
-    }
+    if (tile_lanes_for(max_n) == 1)
+        return launch<SB, 1, V, kPow2>(tb, X, B, T, max_n, rows, n_rows, upr, shift, out, ids,
+                                       lens, err, st);
+    return launch<SB, 2, V, kPow2>(tb, X, B, T, max_n, rows, n_rows, upr, shift, out, ids, lens,
+                                   err, st);
 }
 
 template <typename V, bool kPow2>

@@ -28,9 +28,8 @@ __global__ __launch_bounds__(kTileThreads) void k_pipelined(
     __shared__ int32_t s_tok[TileShape<G>::kPositions + kMaxHalo];
     const int64_t blk = block_index(block0);
     if (blk < n_lookup_blocks) {  // workgroup-uniform
-        // pruned probes: fewer bucket lines compete with the row stream
-        lookup_block<SB, G, (G >= 4)>(slots, mask, X, T, max_n, tiles_per_row, blk, s_tok,
-                                      next_ids, next_len, err);
+        lookup_block<SB, G>(slots, mask, X, T, max_n, tiles_per_row, blk, s_tok, next_ids,
+                            next_len, err);
         return;
     }
     const int64_t r = (blk - n_lookup_blocks) * (kTileThreads / 64) +
@@ -83,12 +82,8 @@ hipError_t by_units(const Step& s, int units) {
 
 template <int SB>
 hipError_t by_lanes(const Step& s, int units) {
-    switch (lanes_for(s.max_n)) {
-        case 1: return by_units<SB, 1>(s, units);
-        case 2: return by_units<SB, 2>(s, units);
-        case 4: return by_units<SB, 4>(s, units);
-        default: return by_units<SB, 8>(s, units);
-    }
+    return tile_lanes_for(s.max_n) == 1 ? by_units<SB, 1>(s, units)
+                                        : by_units<SB, 2>(s, units);
 }
 
 bool overlaps(const void* a, int64_t a_bytes, const void* b, int64_t b_bytes) {

@@ -237,11 +237,10 @@ struct scone_table;
 namespace scone {
 // Launch the lookup kernel (max_n already clamped to the table's K); a null
 // `ids`, `lens` or `hist` output is skipped.  `hist` accumulates, per matched
-// length 1..K, the number of positions (index = length).  `prune` selects
-// the probe schedule of tile_lookup (same results either way).
+// length 1..K, the number of positions (index = length).
 hipError_t launch_lookup(const scone_table* tb, const int32_t* X, int64_t B, int64_t T,
                          int max_n, int32_t* ids, int8_t* lens, unsigned* err, hipStream_t st,
-                         unsigned long long* hist = nullptr, bool prune = false);
+                         unsigned long long* hist = nullptr);
 // Zero `bytes` of device memory with a kernel and raise SCONE_EROW (a table
 // without rows has no valid row id).
 hipError_t launch_zero_rows(void* out, int64_t bytes, unsigned* err, hipStream_t st);

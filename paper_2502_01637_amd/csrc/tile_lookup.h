@@ -13,10 +13,14 @@ struct TileShape {
     static constexpr int kPositions = kTileThreads / G;  // most positions a workgroup can probe
 };
 
-// Lanes per position for a window of max_n: a power of two >= max_n - 1.
+// Lanes per position when every length is probed at once (the decode
+// kernel): a power of two >= max_n - 1.
 __host__ __device__ constexpr int lanes_for(int max_n) {
     return max_n - 1 <= 1 ? 1 : max_n - 1 <= 2 ? 2 : max_n - 1 <= 4 ? 4 : 8;
 }
+
+// Lanes per position of tile_lookup: one for windows up to 2, else two.
+__host__ __device__ constexpr int tile_lanes_for(int max_n) { return max_n <= 2 ? 1 : 2; }
 
 // Stage X[b, t0 - halo .. t0 + P) of one row into LDS (zero outside [0, T));
 // called by the whole workgroup, which then synchronises.
@@ -29,40 +33,40 @@ __device__ __forceinline__ void stage_tokens(int32_t* s_tok, const int32_t* __re
 }
 
 // After stage_tokens and a barrier: position p = threadIdx.x / G (p < P) of
-// the tile gets its longest match.  Lane j of the position's group probes the
-// suffix of length max_n - j.  Without kPrune every length is probed at once.
-// With kPrune, lengths 2 and 3 are probed first; lengths 4 and 5 only when
-// the length-3 suffix has an entry with kExtBit (some f-gram of length >= 4
-// ends with it), and lengths 6 and 7 only when the length-5 suffix does too,
-// so a position stops as soon as no longer f-gram can end there (on a
-// workload of 10M f-grams of length 2..5, 2.75 probes per position instead
-// of 4).  Pruning saves memory traffic but adds dependent rounds, so it pays
-// where many lookups share the memory system (a lookup overlapped with a row
-// stream, a corpus-sized tagging pass) and costs latency where one small
-// lookup runs alone.  A wave ballot then picks the lowest hitting lane (the
-// longest match) and a shuffle brings its id to lane j = 0.  Returns, on lane j = 0 of a valid
+// the tile gets its longest match, G = tile_lanes_for(max_n).  Lane j of the
+// position's pair probes length 3 - j, then 5 - j, then 7 - j (with G = 1
+// the single lane probes length 2).  A round runs only when the previous
+// round's length-3 (length-5) suffix has an entry with kExtBit, i.e. some
+// longer f-gram ends with it, so a position stops as soon as no longer
+// f-gram can end there; the two lanes then compare their longest hits.  On
+// a workload of 10M f-grams of length 2..5 this takes 2.75 probes per
+// position instead of 4.  Two lanes per position, each probing once per
+// round, keep every lane busy: measured against one lane per length (four
+// for max_n = 5, pruned or not), it halved the tagging time and cut the
+// standalone lookup by about a fifth.  Returns, on lane j = 0 of a valid
 // position (p < P, t0 + p < T), the id (or the token itself) and the matched
 // length (1 when nothing matched); `tok_ok` reports whether the position's
 // own token is in range.  All lanes of the wave must call it.
-template <int SB, int G, bool kPrune>
+template <int SB, int G>
 __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __restrict__ slots,
                                             uint64_t mask, const int32_t* s_tok, int64_t T,
                                             int64_t t0, int P, int max_n, int32_t& id_out,
                                             int& len_out, bool& tok_ok) {
+    static_assert(G == 1 || G == 2, "one or two lanes per position");
     const int halo = max_n - 1;
     const int p = threadIdx.x / G;
     const int j = threadIdx.x % G;
     const int64_t t = t0 + p;
     const bool valid = p < P && t < T;
-    const int n = max_n - j;
-    const bool can = valid && n >= 2 && (int64_t)n <= t + 1;
-    const int lane = threadIdx.x & 63;
-    const int base = lane & ~(G - 1);
-    const unsigned group = (1u << G) - 1u;
-    bool hit = false, ext = false;
-    int32_t id = 0;
-    auto probe_here = [&](bool active) {
-        if (!active) return;
+    const int base = (threadIdx.x & 63) & ~(G - 1);
+    const int32_t tok = valid ? s_tok[p + halo] : 0;
+    tok_ok = (tok >= 0) & (tok < SCONE_TOKEN_LIMIT);
+    int best = 0;  // longest f-gram length this lane found
+    int32_t best_id = 0;
+    bool ext = false;  // the last probed key has an entry with kExtBit
+    auto step = [&](int n) {
+        ext = false;
+        if (!(valid && n >= 2 && n <= max_n && (int64_t)n <= t + 1)) return;
         const int32_t* win = s_tok + p + halo - n + 1;  // X[b, t-n+1 .. t]
         bool ok = true;
 #pragma unroll
@@ -70,28 +74,33 @@ __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __
             if (i < n) ok &= (win[i] >= 0) & (win[i] < SCONE_TOKEN_LIMIT);
         int32_t raw = 0;
         if (ok && probe_raw<SB>(slots, mask, pack_key(win, n), raw)) {
-            hit = entry_is_fgram(raw);
-            id = raw & kIdMask;
+            if (entry_is_fgram(raw)) {
+                best = n;
+                best_id = raw & kIdMask;
+            }
             ext = entry_extends(raw);
         }
     };
-    probe_here(can && (n <= 3 || !kPrune));
-    if (kPrune && max_n >= 4) {  // the same for every lane of the launch
-        const bool go4 = ((unsigned)(__ballot(ext && n == 3) >> base) & group) != 0;
-        probe_here(can && go4 && n >= 4 && n <= 5);
+    step(G == 2 ? 3 - j : 2);
+    if (max_n >= 4) {  // the same for every lane of the launch
+        const bool go4 = __shfl((int)ext, base) != 0;  // lane j = 0 probed length 3
+        if (go4) step(5 - j);
+        else ext = false;
         if (max_n >= 6) {
-            const bool go6 = ((unsigned)(__ballot(ext && n == 5) >> base) & group) != 0;
-            probe_here(can && go6 && n >= 6);
+            const bool go6 = __shfl((int)ext, base) != 0;  // and then length 5
+            if (go6) step(7 - j);
         }
     }
-    const unsigned long long m = __ballot(hit);
-    const unsigned gm = (unsigned)(m >> base) & group;
-    const int jb = gm ? __ffs(gm) - 1 : 0;
-    const int32_t best = __shfl(id, base + jb);
-    const int32_t tok = valid ? s_tok[p + halo] : 0;
-    tok_ok = (tok >= 0) & (tok < SCONE_TOKEN_LIMIT);
-    id_out = gm ? best : tok;
-    len_out = gm ? max_n - jb : 1;
+    if (G == 2) {
+        const int ob = __shfl_xor(best, 1);
+        const int32_t oid = __shfl_xor(best_id, 1);
+        if (ob > best) {
+            best = ob;
+            best_id = oid;
+        }
+    }
+    id_out = best ? best_id : tok;
+    len_out = best ? best : 1;
 }
 
 // One workgroup's share of a lookup over X [B, T]: tile `tile` of the row-major
@@ -100,7 +109,7 @@ __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __
 // length (either output may be null); a bad token raises SCONE_ETOKEN.
 // Returns the matched length on the lane that wrote a position, else 0.
 // Called by the whole workgroup (it synchronises once).
-template <int SB, int G, bool kPrune>
+template <int SB, int G>
 __device__ __forceinline__ int lookup_block(const typename SlotOps<SB>::Slot* __restrict__ slots,
                                             uint64_t mask, const int32_t* __restrict__ X,
                                             int64_t T, int max_n, int64_t tiles_per_row,
@@ -116,7 +125,7 @@ __device__ __forceinline__ int lookup_block(const typename SlotOps<SB>::Slot* __
     int32_t id;
     int len;
     bool tok_ok;
-    tile_lookup<SB, G, kPrune>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok);
+    tile_lookup<SB, G>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok);
     const int64_t t = t0 + threadIdx.x / G;
     if (threadIdx.x % G == 0 && t < T) {
         if (!tok_ok) atomicOr(err, err_bit(SCONE_ETOKEN));
