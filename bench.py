@@ -12,9 +12,20 @@ JSON line with tokens/s, the step kernel's achieved bandwidth against its
 roofline (HBM, or PCIe when the rows live in host-pinned memory), and the CPU
 oracle timed on a bounded sample of the same workload.
 
-Workloads (``--config``): c2_1m (default), c3_10m_k5, tiny (HBM prefill),
-c4_host (rows in host-pinned memory read over PCIe), c5_decode (256
-sequences x 1024 decoding steps of one token each).
+Workloads (``--config``): c3_10m_k5 (default: 10M f-grams of length 2..5,
+4 KiB rows, 41 GB in HBM, the largest workload one GPU holds), c2_1m, tiny
+(HBM prefill), c4_host (rows in host-pinned memory read over PCIe), c5_decode
+(256 sequences x 1024 decoding steps of one token each).
+
+The headline roofline fraction is cache-assisted: Zipf-distributed ids repeat
+rows that the L2s and the 256 MB last-level cache then serve.  The same
+pipelined step over uniform random ids (no repeated rows) is reported beside
+it as ``roofline.no_reuse``.
+
+Profiling: ``--plan-out FILE`` records which library kernel each dispatch of
+the run is and to which phase it belongs; ``--reduce-trace`` and
+``--reduce-counters`` turn rocprofv3 csv output of such a run into the
+summaries under profiles/ (see ``reduce_main``).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config NAME]
 """
@@ -37,7 +48,7 @@ METRIC = "tokens/sec and gather GB/s (% of HBM peak) for f-gram lookup+gather, 1
 HBM_PEAK_GBPS = 8000.0
 PCIE_PEAK_GBPS = 63.0    # PCIe 5.0 x16, one direction
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16 matrix-core peak
-DEFAULT_CONFIG = "c2_1m"
+DEFAULT_CONFIG = "c3_10m_k5"
 N_BATCHES = 4
 SAMPLE_EVERY = 8
 COLD_REPS = 10
@@ -60,9 +71,10 @@ def describe(cfg) -> str:
 # The sources of each measured kernel (its file and the headers that hold its
 # device code): a traffic summary is used only while they are unchanged.
 KERNEL_SOURCES = {
-    "gather": ("gather.hip", "row_copy.h"),
-    "embed": ("embed.hip", "tile_lookup.h"),
-    "pipelined": ("pipeline.hip", "row_copy.h", "tile_lookup.h"),
+    "gather": ("gather.hip", "row_copy.h", "scone_internal.h"),
+    "embed": ("embed.hip", "tile_lookup.h", "scone_internal.h", "table_build.hip"),
+    "pipelined": ("pipeline.hip", "row_copy.h", "tile_lookup.h", "scone_internal.h",
+                  "table_build.hip"),
 }
 
 
@@ -183,9 +195,98 @@ def split_placement(S, torch, cfg, table, rows, X, fid, outs, K, warmup):
             "rows_equal_plain_gather": same}
 
 
+class Plan:
+    """The library kernels a run launches, one entry per dispatch, in order,
+    each with the phase it belongs to.  ``--plan-out`` writes it next to a
+    rocprofv3 run so that the reducers can tell the timed dispatches of each
+    phase apart from warm-up, control and parity launches."""
+
+    def __init__(self):
+        self.entries = []
+
+    def add(self, phase: str, kernel: str, n: int = 1):
+        self.entries.extend([[phase, kernel]] * n)
+
+
+PLAN = Plan()
+
+
+def host_info() -> dict:
+    """CPU model and the cores this process may run on."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    return {"cpu_model": model, "cores_available": int(cores or 1)}
+
+
+def oracle_threads() -> int:
+    """Threads for the all-core oracle timing: the cores this process may use,
+    capped by OMP_NUM_THREADS when the environment sets it."""
+    n = host_info()["cores_available"]
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        n = min(n, int(env))
+    return max(1, n)
+
+
+def probes_per_position(cfg, w, X: np.ndarray) -> float:
+    """Mean hash probes per position of the kernels' tile lookup, counted on
+    the host by replaying its schedule (not read off the device): lengths 3
+    and 2 in the first round (only 2 when max_n = 2), 5 and 4 in the second
+    where the length-3 suffix ends some f-gram of length 4 or more, 7 and 6 in
+    the third where the length-5 suffix ends one of length 6 or more; a length
+    is probed only when it fits the window (n <= min(max_n, t + 1))."""
+    B, T = X.shape
+    max_n = min(cfg.max_n, cfg.max_len)     # the library clamps the window to K
+    top = np.broadcast_to(np.minimum(max_n, np.arange(T) + 1), (B, T))
+
+    def fits(n):
+        return (top >= n) if n >= 2 else np.zeros_like(top, dtype=bool)
+
+    def windows(n):
+        """The length-n window ending at every position, as n int32 tokens in
+        one opaque value (positions before t = n - 1 get zeros, and fits()
+        masks them)."""
+        win = np.zeros((B, T, n), dtype=np.int32)
+        for i in range(n):
+            lag = n - 1 - i                       # token i of the window is X[t - lag]
+            win[:, lag:, i] = X[:, :T - lag]
+        return win.reshape(B * T, n).view(np.dtype((np.void, 4 * n))).reshape(B, T)
+
+    def flagged(n):
+        """Positions whose length-n suffix ends an f-gram longer than n + 1."""
+        long_ = w.lengths >= n + 1
+        if not long_.any():
+            return np.zeros((B, T), dtype=bool)
+        sel = w.fgrams[long_]
+        L = w.lengths[long_].astype(np.int64)
+        cols = L[:, None] - n + np.arange(n)[None, :]
+        ends = np.ascontiguousarray(np.take_along_axis(sel, cols, axis=1), dtype=np.int32)
+        ends = ends.view(np.dtype((np.void, 4 * n))).ravel()
+        return np.isin(windows(n), np.unique(ends)) & fits(n)
+
+    if max_n <= 2:
+        return float(fits(2).sum()) / X.size
+    probes = fits(3).astype(np.int64) + fits(2).astype(np.int64)
+    if max_n >= 4:
+        go = flagged(3)
+        probes += go * (fits(5).astype(np.int64) + fits(4))
+        if max_n >= 6:
+            probes += (go & flagged(5)) * (fits(7).astype(np.int64) + fits(6))
+    return float(probes.sum()) / X.size
+
+
 def cpu_baseline(cfg, w, X0, host_np_full, E, gpu_ids, gpu_outs, min_seconds: float):
     """Time the oracle (single-threaded) on batch 0, repeated until min_seconds,
-    and check the GPU results of batch 0 against it."""
+    then the same passes split by rows over all host cores (labelled), and
+    check the GPU results of batch 0 against it."""
+    import threading
     import torch
     import oracle
     from workloads import table_rows
@@ -193,6 +294,7 @@ def cpu_baseline(cfg, w, X0, host_np_full, E, gpu_ids, gpu_outs, min_seconds: fl
     o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
     build_s = time.perf_counter() - t0
     exp_ids, exp_len = o.lookup(X0, cfg.max_n)
+    queries = o.queries
     uniq = None
     if host_np_full is not None:
         host_np, what = host_np_full, "the full host-pinned table"
@@ -205,27 +307,53 @@ def cpu_baseline(cfg, w, X0, host_np_full, E, gpu_ids, gpu_outs, min_seconds: fl
         host = table_rows(cfg, torch.from_numpy(uniq.astype(np.int64)), device="cuda").cpu()
         host_np = host.view(torch.uint8).numpy()
         what = f"a compact host table of the {len(uniq)} referenced rows (id remap timed)"
+
+    def one_pass(rows):
+        ids_p, _ = o.lookup(rows, cfg.max_n)
+        if uniq is not None:
+            ids_p = np.searchsorted(uniq, ids_p).astype(np.int32)
+        return oracle.gather(ids_p, host_np)
+
     passes, elapsed = 0, 0.0
     while elapsed < min_seconds or passes == 0:
         t = time.perf_counter()
-        ids_p, _ = o.lookup(X0, cfg.max_n)
-        if uniq is not None:
-            ids_p = np.searchsorted(uniq, ids_p).astype(np.int32)
-        out = oracle.gather(ids_p, host_np)
+        out = one_pass(X0)
         elapsed += time.perf_counter() - t
         passes += 1
+    # All host cores: the rows of batch 0 split into one slice per thread
+    # (the oracle's calls release the interpreter lock, so slices run in
+    # parallel on a shared read-only dictionary).
+    nthr = min(oracle_threads(), X0.shape[0])
+    slices = np.array_split(np.arange(X0.shape[0]), nthr)
+    mt_passes, mt_elapsed = 0, 0.0
+    while mt_elapsed < min_seconds / 2 or mt_passes == 0:
+        t = time.perf_counter()
+        th = [threading.Thread(target=one_pass, args=(X0[sl],)) for sl in slices]
+        for x in th:
+            x.start()
+        for x in th:
+            x.join()
+        mt_elapsed += time.perf_counter() - t
+        mt_passes += 1
     parity_rows = [bool(g.view(torch.uint8).cpu().numpy().reshape(out.shape).tobytes()
                         == out.tobytes()) for g in gpu_outs]
+    info = host_info()
     return ({"value": passes * cfg.n_tok / elapsed, "unit": "tokens/s", "cores": 1,
              "kind": "oracle",
              "sample": f"batch 0 ({cfg.n_tok} tokens) of {describe(cfg)}; {passes} full "
                        f"passes of lookup + memcpy gather from {what}; dictionary build "
                        f"({build_s:.1f} s) not timed",
-             "seconds": round(elapsed, 3), "build_seconds": round(build_s, 3)},
+             "seconds": round(elapsed, 3), "build_seconds": round(build_s, 3),
+             "cpu_model": info["cpu_model"], "cores_available": info["cores_available"],
+             "all_cores": {"value": mt_passes * cfg.n_tok / mt_elapsed, "unit": "tokens/s",
+                           "threads": nthr, "passes": mt_passes,
+                           "seconds": round(mt_elapsed, 3),
+                           "how": "the same passes with the rows of batch 0 split over "
+                                  f"{nthr} threads sharing the oracle's dictionary"}},
             {"ids_bit_exact": bool(np.array_equal(gpu_ids, exp_ids)),
              "split_rows_bit_exact": parity_rows[0], "fused_rows_bit_exact": parity_rows[1],
              "pipelined_rows_bit_exact": parity_rows[2],
-             "positions": int(cfg.n_tok)}, exp_len)
+             "positions": int(cfg.n_tok)}, exp_len, queries)
 
 
 def run_prefill(args, cfg):
@@ -257,12 +385,12 @@ def run_prefill(args, cfg):
     # dirty there and every step's writes reach HBM.
     outs = [torch.empty((cfg.B, cfg.T, cfg.d), dtype=torch_dtype(cfg), device=dev)
             for _ in range(N_BATCHES)]
-    out = outs[0]
     torch.cuda.synchronize()
-    log(f"table: {table.n} f-grams, {table.capacity} slots x {table.slot_bytes} B, "
-        f"build {build_s * 1e3:.1f} ms")
+    log(f"table: {table.n} f-grams, {table.entries} entries in {table.capacity} slots x "
+        f"{table.slot_bytes} B, build {build_s * 1e3:.1f} ms")
 
     K = args.steps
+    G = "k_gather"      # k_gather_rows for whole-KiB rows, k_gather otherwise
 
     def pipelined_step(g):
         S.embed_pipelined(table, X[(g + 1) % N_BATCHES], cfg.max_n, pid[(g + 1) % 2],
@@ -272,17 +400,22 @@ def run_prefill(args, cfg):
         """W warm-up steps, then K timed steps between two synchronisations.
         HIP events around each kernel are recorded on every 8th step only, so
         that they barely perturb the wall clock.  Returns (wall seconds,
-        per-kernel mean ms list)."""
+        per-kernel mean ms list, device ms per step over the timed region)."""
         if path == "pipelined":   # first lookup, before the warm-up steps
             S.embed_pipelined(table, X[0], cfg.max_n, pid[0], None, rows)
+            PLAN.add("pipelined_first_lookup", "k_lookup")
         for k in range(args.warmup):
             if path == "split":
                 S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
                 S.gather(fid, rows, out=outs[k % N_BATCHES])
+                PLAN.add("serial_warmup", "k_lookup")
+                PLAN.add("serial_warmup", G)
             elif path == "pipelined":
                 pipelined_step(k)
+                PLAN.add("pipelined_warmup", "k_pipelined")
             else:
                 S.embed(table, X[k % N_BATCHES], cfg.max_n, rows, out=outs[k % N_BATCHES])
+                PLAN.add("fused_warmup", "k_embed")
         rc = S.check()
         if rc != 0:
             raise SystemExit(f"device error after warmup ({path}): status {rc}")
@@ -303,10 +436,14 @@ def run_prefill(args, cfg):
                 if e:
                     e[1].record()
                 S.gather(fid, rows, out=outs[k % N_BATCHES])
+                PLAN.add("serial_timed", "k_lookup")
+                PLAN.add("serial_timed", G)
             elif path == "pipelined":
                 pipelined_step(args.warmup + k)
+                PLAN.add("pipelined_timed", "k_pipelined")
             else:
                 S.embed(table, X[k % N_BATCHES], cfg.max_n, rows, out=outs[k % N_BATCHES])
+                PLAN.add("fused_timed", "k_embed")
             if e:
                 e[nk].record()
         span[1].record()
@@ -336,11 +473,10 @@ def run_prefill(args, cfg):
     pipe_achieved = pipe_bytes / (pipe_ms * 1e-3) / 1e9
     value = cfg.n_tok * K / wall
 
-    # Two controls at the same shape, each rotating N_BATCHES distinct id sets
-    # like the query batches (one set reused every step would leave its rows
-    # in the 256 MB last-level cache): uniform random ids (no Zipf reuse to
-    # help the caches) and contiguous rows (the kernel's streaming rate with
-    # neither reuse nor random access).
+    # Id sets without reuse, rotated like the query batches (one set reused
+    # every step would leave its rows in the 256 MB last-level cache):
+    # uniform random ids over the whole table, and contiguous rows (the
+    # kernel's streaming rate with neither reuse nor random access).
     gen = torch.Generator(device=dev)
     gen.manual_seed(cfg.seed)
     uids = [torch.randint(0, cfg.n_rows, (cfg.B, cfg.T), dtype=torch.int32, device=dev,
@@ -348,9 +484,31 @@ def run_prefill(args, cfg):
     sids = [(torch.arange(k * cfg.n_tok, (k + 1) * cfg.n_tok, dtype=torch.int64, device=dev)
              % cfg.n_rows).to(torch.int32).view(cfg.B, cfg.T) for k in range(N_BATCHES)]
 
-    def control_ms(idsets):
+    # The headline kernel without cache help: the same pipelined steps, each
+    # looking up the next real batch while it gathers one of the uniform id
+    # sets.  Its rate is HBM's alone.
+    nr_next = torch.empty_like(pid[0])
+    for k in range(2):
+        S.embed_pipelined(table, X[(k + 1) % N_BATCHES], cfg.max_n, nr_next,
+                          uids[k % N_BATCHES], rows, out=outs[k % N_BATCHES])
+    PLAN.add("noreuse_warmup", "k_pipelined", 2)
+    torch.cuda.synchronize()
+    ne = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ne[0].record()
+    for k in range(K):
+        S.embed_pipelined(table, X[(k + 1) % N_BATCHES], cfg.max_n, nr_next,
+                          uids[k % N_BATCHES], rows, out=outs[k % N_BATCHES])
+    ne[1].record()
+    torch.cuda.synchronize()
+    PLAN.add("noreuse_timed", "k_pipelined", K)
+    if S.check() != 0:
+        raise SystemExit("device error in the no-reuse pipelined steps")
+    noreuse_ms = ne[0].elapsed_time(ne[1]) / K
+
+    def control_ms(idsets, phase):
         for k in range(2):
             S.gather(idsets[k % N_BATCHES], rows, out=outs[k % N_BATCHES])
+        PLAN.add(phase + "_warmup", G, 2)
         torch.cuda.synchronize()
         ue = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         ue[0].record()
@@ -358,11 +516,12 @@ def run_prefill(args, cfg):
             S.gather(idsets[k % N_BATCHES], rows, out=outs[k % N_BATCHES])
         ue[1].record()
         torch.cuda.synchronize()
+        PLAN.add(phase + "_timed", G, K)
         return ue[0].elapsed_time(ue[1]) / K
 
-    uniform_ms = control_ms(uids)
-    sequential_ms = control_ms(sids)
-    del uids, sids
+    uniform_ms = control_ms(uids, "uniform")
+    sequential_ms = control_ms(sids, "contiguous")
+    del uids, sids, nr_next
 
     # Cold caches: reading a 1 GiB buffer between repetitions evicts the L2s
     # and the 256 MB last-level cache, so table, hash slots and tokens all come
@@ -381,7 +540,10 @@ def run_prefill(args, cfg):
             S.gather(fid, rows, out=outs[k % N_BATCHES])
             e[2].record()
             ce.append(e)
+            PLAN.add("cold_serial", "k_lookup")
+            PLAN.add("cold_serial", G)
         S.embed_pipelined(table, X[0], cfg.max_n, pid[0], None, rows)
+        PLAN.add("cold_first_lookup", "k_lookup")
         for k in range(COLD_REPS):
             flush.amax()
             e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
@@ -389,6 +551,7 @@ def run_prefill(args, cfg):
             pipelined_step(k)
             e[1].record()
             pe.append(e)
+            PLAN.add("cold_pipelined", "k_pipelined")
         torch.cuda.synchronize()
         del flush
         c_look = float(np.mean([e[0].elapsed_time(e[1]) for e in ce]))
@@ -417,6 +580,11 @@ def run_prefill(args, cfg):
     out0f = S.embed(table, X[0], cfg.max_n, rows)
     S.embed_pipelined(table, X[0], cfg.max_n, pid[0], None, rows)
     out0p = S.embed_pipelined(table, X[1], cfg.max_n, pid[1], pid[0], rows)
+    PLAN.add("parity", "k_lookup")
+    PLAN.add("parity", G)
+    PLAN.add("parity", "k_embed")
+    PLAN.add("parity", "k_lookup")
+    PLAN.add("parity", "k_pipelined")
     if S.check() != 0:
         raise SystemExit("device error in parity pass")
     torch.cuda.synchronize()
@@ -433,10 +601,12 @@ def run_prefill(args, cfg):
                  "pct_of_h2d_ceiling": 100.0 * pcie / ceiling,
                  "pcie_inclusive_tokens_per_s": value, "split_placement": split}
         alg_bytes = read_bytes
+        nr_rate = read_bytes / (noreuse_ms * 1e-3) / 1e9
     else:
         bound, peak, rate = "hbm", HBM_PEAK_GBPS, pipe_achieved
         extra = {}
         alg_bytes = pipe_bytes
+        nr_rate = pipe_bytes / (noreuse_ms * 1e-3) / 1e9
 
     def control(ms):
         """A gather control's rate: HBM bytes against the HBM peak, or for
@@ -466,7 +636,7 @@ def run_prefill(args, cfg):
                    "n_fgrams": cfg.n_fgrams, "max_n": cfg.max_n, "d": cfg.d,
                    "row_bytes": cfg.row_bytes, "placement": cfg.placement,
                    "hash_slots": table.capacity, "slot_bytes": table.slot_bytes,
-                   "rotating_batches": N_BATCHES},
+                   "max_load": args.max_load, "rotating_batches": N_BATCHES},
         "path": "scone_embed_pipelined (one launch per step: gather of batch k, lookup of "
                 "batch k+1)",
         "pipelined_us": pipe_ms * 1e3,
@@ -491,10 +661,23 @@ def run_prefill(args, cfg):
         "traffic": None if traffic is None else traffic["traffic_bytes_per_launch"],
         "kernel": "scone_embed_pipelined (k_pipelined)",
         "algorithmic_bytes_per_launch": alg_bytes,
+        "cache_assisted": True,
+        "note": "frac counts algorithmic bytes over the step time on the Zipf workload, whose "
+                "repeated rows the L2s and the 256 MB last-level cache serve in part; "
+                "no_reuse is the same kernel over uniform random ids; traffic is L2-miss "
+                "bytes (FETCH_SIZE + WRITE_SIZE, calibrated), which include last-level-cache "
+                "hits: gfx950's counters do not separate DRAM from that cache",
+        "no_reuse": {"achieved": nr_rate, "frac": nr_rate / peak, "us": noreuse_ms * 1e3,
+                     "traffic": None if traffic is None
+                     else traffic.get("noreuse_traffic_bytes_per_launch"),
+                     "ids": f"uniform random over all {cfg.n_rows} rows, {N_BATCHES} "
+                            "rotating sets; the lookup half runs on the real next batch"},
     }
     gtraffic = measured_traffic(cfg.name, "gather")
     result["serial_path"]["gather_traffic"] = (None if gtraffic is None
                                                else gtraffic["traffic_bytes_per_launch"])
+    result["uniform_id_gather"]["traffic"] = (None if gtraffic is None
+                                              else gtraffic.get("uniform_traffic_bytes_per_launch"))
     etraffic = measured_traffic(cfg.name, "embed")
     result["fused_path"]["traffic"] = (None if etraffic is None
                                        else etraffic["traffic_bytes_per_launch"])
@@ -504,19 +687,28 @@ def run_prefill(args, cfg):
                        "hash_table_bytes": table.capacity * table.slot_bytes,
                        "total_bytes": cfg.n_rows * cfg.row_bytes
                        + table.capacity * table.slot_bytes,
-                       "hash_load": table.n / table.capacity}
+                       "hash_load": table.entries / table.capacity,
+                       "hash_entries": table.entries, "fgrams": table.n,
+                       "suffix_entries": table.entries - table.n}
     ml = ml0.cpu().numpy()
     result["match"] = match_stats(ml, cfg.max_n)
     result["build_ms"] = build_s * 1e3
+    result["probes"] = {
+        "per_position_kernel_schedule": probes_per_position(cfg, w, batches_np[0]),
+        "counted": "on the host, replaying the tile lookup's pruned two-lane schedule over "
+                   "batch 0 (each probe reads one 64-byte bucket, more only when it is full)",
+        "max_per_position": max(cfg.max_n - 1, 0)}
 
     if not args.no_cpu_baseline:
         host_np = rows.tensor().view(torch.uint8).numpy() if host else None
-        cb, parity, exp_len = cpu_baseline(cfg, w, batches_np[0], host_np, E,
-                                           fid0.cpu().numpy(), [out0, out0f, out0p],
-                                           args.cpu_seconds)
+        cb, parity, exp_len, queries = cpu_baseline(cfg, w, batches_np[0], host_np, E,
+                                                    fid0.cpu().numpy(), [out0, out0f, out0p],
+                                                    args.cpu_seconds)
         parity["match_len_bit_exact"] = bool(np.array_equal(ml, exp_len))
         result["cpu_baseline"] = cb
         result["parity"] = parity
+        result["probes"]["oracle_queries_per_position"] = queries / cfg.n_tok
+        result["probes"]["oracle_order"] = "longest first, stop at the first hit"
     else:
         result["cpu_baseline"] = None
     if host:
@@ -932,7 +1124,228 @@ def run_precompute(args, cfg):
     return result
 
 
+# ------------------------------------------------------------ profiles ----
+# rocprofv3 writes one csv row per dispatch (kernel trace) or per dispatch and
+# counter (counter collection).  A run made with --plan-out also leaves the
+# plan of its library dispatches; the reducers below walk the csv's library
+# kernels in dispatch order against that plan, so each figure is taken over
+# the timed dispatches of one phase only.
+
+BUILD_KERNELS = ("k_count_long", "k_insert", "k_verify", "k_mark", "k_count_used")
+
+
+def _short(name: str) -> str:
+    n = re.sub(r"\(anonymous namespace\)::", "", name)
+    return n.split("(")[0].replace("void ", "").replace("scone::", "").strip()
+
+
+def _library_dispatches(rows):
+    """This library's dispatches after the table build, in dispatch order."""
+    lib = sorted((r for r in rows if "scone::" in r["Kernel_Name"]),
+                 key=lambda r: int(r["Dispatch_Id"]))
+    i = 0
+    while i < len(lib) and _short(lib[i]["Kernel_Name"]).startswith(BUILD_KERNELS):
+        i += 1
+    return lib[i:]
+
+
+def _by_phase(rows, plan):
+    """{phase: [row, ...]} after checking every dispatch against the plan."""
+    lib = _library_dispatches(rows)
+    if len(lib) < len(plan["entries"]):
+        raise SystemExit(f"the csv has {len(lib)} library dispatches after the build, "
+                         f"the plan {len(plan['entries'])}")
+    out = {}
+    for (phase, kernel), r in zip(plan["entries"], lib):
+        if not _short(r["Kernel_Name"]).startswith(kernel):
+            raise SystemExit(f"dispatch {r['Dispatch_Id']} is {_short(r['Kernel_Name'])}, "
+                             f"the plan expects {kernel} ({phase})")
+        out.setdefault(phase, []).append(r)
+    return out
+
+
+def _read_csv(path):
+    import csv
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def reduce_trace(trace_csv, plan_path, bench_json, out_md, profile_cmd):
+    """profiles/<workload>_kernel_trace.md from a --kernel-trace run."""
+    import statistics as st
+    plan = json.load(open(plan_path))
+    rows = _read_csv(trace_csv)
+    for r in rows:
+        r["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    ph = _by_phase(rows, plan)
+    bench = None
+    for line in (open(bench_json) if bench_json else []):
+        if line.startswith('{"metric"'):
+            bench = json.loads(line)
+    lib = [r for r in rows if "scone::" in r["Kernel_Name"]]
+    by = {}
+    for r in lib:
+        by.setdefault(_short(r["Kernel_Name"]), []).append(r)
+    us = lambda L: st.mean(x["ns"] for x in L) / 1e3
+    med = lambda L: st.median(x["ns"] for x in L) / 1e3
+    span = lambda L: f"{L[0]['Dispatch_Id']}-{L[-1]['Dispatch_Id']}"
+    cfgname = plan["config"]
+    srcs = sorted({s for v in KERNEL_SOURCES.values() for s in v} | {"lookup.hip"})
+    L = [f"# Kernel trace: {cfgname} ({plan['workload']})\n",
+         "Command (one MI355X, `<repo>` the repository root):\n", f"    {profile_cmd}\n",
+         "Reduced with `python bench.py --reduce-trace <out>/run_kernel_trace.csv "
+         "--plan <plan.json> --bench-json <bench stdout> --out <this file>`.\n",
+         "Per-kernel durations from the kernel-trace csv (ns); only this library's kernels.",
+         "Sources (sha1): " + ", ".join(f"{s} {source_sha(s)}" for s in srcs) + ".\n", "```"]
+    for name, rs in sorted(by.items(), key=lambda kv: -sum(x["ns"] for x in kv[1])):
+        ns = [x["ns"] for x in rs]
+        r0 = rs[0]
+        L.append(f"{name[:58]:58s} calls={len(rs):4d} avg_ns={st.mean(ns):11.1f} "
+                 f"med_ns={st.median(ns):10.1f} min_ns={min(ns):9d} max_ns={max(ns):9d} "
+                 f"grid={r0['Grid_Size_X']} wg={r0['Workgroup_Size_X']} vgpr={r0['VGPR_Count']} "
+                 f"lds={r0['LDS_Block_Size']}")
+    L += ["```\n", f"By phase ({plan['steps']} timed steps each; dispatch numbers from the csv):\n",
+          "```"]
+    for phase in ("pipelined_timed", "noreuse_timed", "serial_timed", "fused_timed",
+                  "uniform_timed", "contiguous_timed", "cold_serial", "cold_pipelined"):
+        if phase not in ph:
+            continue
+        groups = {}
+        for r in ph[phase]:
+            groups.setdefault(_short(r["Kernel_Name"]), []).append(r)
+        for name, rs in groups.items():
+            L.append(f"{phase:17s} {name[:40]:40s} n={len(rs):3d} (dispatches {span(rs)}) "
+                     f"mean {us(rs):8.2f} us  median {med(rs):8.2f} us")
+    L.append("```\n")
+    if bench:
+        L.append("bench.py's own figures in the same run (HIP events, under the profiler): "
+                 f"pipelined step {bench['pipelined_us']:.1f} us (device time of the timed "
+                 f"region per step), no-reuse pipelined step "
+                 f"{bench['roofline']['no_reuse']['us']:.1f} us, serial lookup "
+                 f"{bench['lookup_us']:.1f} us + gather {bench['gather_us']:.1f} us, "
+                 f"uniform-id gather {bench['uniform_id_gather']['us']:.1f} us, contiguous "
+                 f"rows {bench['sequential_row_gather']['us']:.1f} us; headline "
+                 f"{bench['value'] / 1e9:.3f} G tokens/s, roofline frac "
+                 f"{bench['roofline']['frac']:.3f} (no reuse "
+                 f"{bench['roofline']['no_reuse']['frac']:.3f}).\n")
+    open(out_md, "w").write("\n".join(L) + "\n")
+    print(f"wrote {out_md}")
+
+
+def reduce_counters(fetch_csv, write_csv, plan_path, fetch_cmd, write_cmd, out_dir):
+    """profiles/<kernel>_<workload>_traffic.md from a FETCH_SIZE run and a
+    WRITE_SIZE run of the same bench.py command (with --copy-calibration)."""
+    import statistics as st
+    from workloads import CONFIGS
+    plan = json.load(open(plan_path))
+    cfgname = plan["config"]
+    cfg = CONFIGS[cfgname]
+    per = {}
+    copies = {}
+    for ctr, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = [r for r in _read_csv(path) if r["Counter_Name"] == ctr]
+        per[ctr] = _by_phase(rows, plan)
+        cp = sorted((r for r in rows if "copyBuffer" in r["Kernel_Name"]),
+                    key=lambda r: int(r["Dispatch_Id"]))
+        big = max(int(r["Grid_Size"]) for r in cp)
+        copies[ctr] = [float(r["Counter_Value"]) for r in cp if int(r["Grid_Size"]) == big][-5:]
+    kib = plan["copy_calibration_mib"] * 1024.0
+    fscale = kib / st.mean(copies["FETCH_SIZE"])
+    wscale = kib / st.mean(copies["WRITE_SIZE"])
+
+    def mean_kib(ctr, phase, kernel):
+        v = [float(r["Counter_Value"]) for r in per[ctr].get(phase, [])
+             if _short(r["Kernel_Name"]).startswith(kernel)]
+        return st.mean(v) if v else None
+
+    def traffic(phase, kernel):
+        f, w = mean_kib("FETCH_SIZE", phase, kernel), mean_kib("WRITE_SIZE", phase, kernel)
+        if f is None or w is None:
+            return None, None, None
+        return f, w, int(round(f * 1024 * fscale + w * 1024 * wscale))
+
+    G = "k_gather"
+    specs = {
+        "pipelined": ("k_pipelined", [("pipelined_timed", "traffic_bytes_per_launch", "Zipf workload"),
+                                      ("noreuse_timed", "noreuse_traffic_bytes_per_launch",
+                                       "uniform random ids (no reuse)")],
+                      cfg.gather_bytes() + cfg.n_tok * 8,
+                      f"2 x {cfg.row_bytes} B rows + 4 B id read + 4 B token read + 4 B id written"),
+        "gather": (G, [("serial_timed", "traffic_bytes_per_launch", "Zipf workload"),
+                       ("uniform_timed", "uniform_traffic_bytes_per_launch",
+                        "uniform random ids (no reuse)"),
+                       ("contiguous_timed", "contiguous_traffic_bytes_per_launch",
+                        "contiguous rows")],
+                   cfg.gather_bytes(), f"2 x {cfg.row_bytes} B rows + 4 B id"),
+        "embed": ("k_embed", [("fused_timed", "traffic_bytes_per_launch", "Zipf workload")],
+                  cfg.gather_bytes(), f"4 B token + 2 x {cfg.row_bytes} B rows"),
+    }
+    lf, lw, lt = traffic("serial_timed", "k_lookup")
+    for key, (kernel, phases, alg, algtxt) in specs.items():
+        rec = {"config": cfgname, "kernel": kernel, "source_sha1": source_sha(*KERNEL_SOURCES[key]),
+               "fetch_scale": round(fscale, 5), "write_scale": round(wscale, 5)}
+        lines = []
+        for phase, field, what in phases:
+            f, w, t = traffic(phase, kernel)
+            if t is None:
+                continue
+            rec[field] = t
+            if field == "traffic_bytes_per_launch":
+                rec["fetch_kib_per_dispatch"] = round(f, 1)
+                rec["write_kib_per_dispatch"] = round(w, 1)
+            lines.append(f"{phase:17s} ({what}): FETCH_SIZE {f:10.1f} KiB x {fscale:.4f} + "
+                         f"WRITE_SIZE {w:10.1f} KiB x {wscale:.4f} = {t / 1e6:8.1f} MB per launch")
+        L = [f"# L2-miss traffic of {kernel} on {cfgname} ({plan['workload']})\n",
+             "Two counter passes, each its own run of the same command (one MI355X):\n",
+             f"    {fetch_cmd}", f"    {write_cmd}\n",
+             "Reduced with `python bench.py --reduce-counters <fetch csv> <write csv> "
+             "--plan <plan.json>`.\n",
+             "FETCH_SIZE and WRITE_SIZE count the bytes the L2s request from and write to "
+             "the memory fabric.  On MI355X the 256 MB last-level cache (Infinity Cache) sits "
+             "behind that fabric, so these are L2-miss bytes: they include last-level-cache "
+             "hits, and no counter gfx950 exposes to rocprofv3 separates DRAM traffic from "
+             "them (its counter list has no data-fabric or memory-controller block).  With "
+             "uniform random ids over a table far larger than that cache the two coincide.\n",
+             f"Calibration: the run's last five plain device copies of "
+             f"{plan['copy_calibration_mib']} MiB read FETCH_SIZE = "
+             f"{st.mean(copies['FETCH_SIZE']):.1f} KiB and WRITE_SIZE = "
+             f"{st.mean(copies['WRITE_SIZE']):.1f} KiB for {kib:.0f} KiB moved each way, so "
+             f"FETCH_SIZE is scaled by {fscale:.4f} and WRITE_SIZE by {wscale:.4f}.\n",
+             f"Means over each phase's {plan['steps']} timed dispatches:\n", "```"] + lines + [
+             "```\n",
+             f"Algorithmic bytes per launch: {alg / 1e6:.1f} MB ({cfg.n_tok} tokens x "
+             f"({algtxt})).",
+             (f"The standalone lookup kernel moves {lt / 1e6:.1f} MB per launch in the same run "
+              f"(FETCH {lf:.1f} KiB, WRITE {lw:.1f} KiB).\n" if lt else ""),
+             "TRAFFIC " + json.dumps(rec)]
+        out = os.path.join(out_dir, f"{key}_{cfgname}_traffic.md")
+        open(out, "w").write("\n".join(L) + "\n")
+        print(f"wrote {out}")
+
+
+def reduce_main(argv):
+    ap = argparse.ArgumentParser(description="reduce rocprofv3 csv output of a bench.py run")
+    ap.add_argument("--reduce-trace", metavar="KERNEL_TRACE_CSV")
+    ap.add_argument("--reduce-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
+    ap.add_argument("--plan", required=True)
+    ap.add_argument("--bench-json")
+    ap.add_argument("--out")
+    ap.add_argument("--profile-cmd", default="", help="the profiler command (trace)")
+    ap.add_argument("--fetch-cmd", default="")
+    ap.add_argument("--write-cmd", default="")
+    ap.add_argument("--out-dir", default=os.path.join(ROOT, "profiles"))
+    a = ap.parse_args(argv)
+    if a.reduce_trace:
+        reduce_trace(a.reduce_trace, a.plan, a.bench_json, a.out, a.profile_cmd)
+    if a.reduce_counters:
+        reduce_counters(a.reduce_counters[0], a.reduce_counters[1], a.plan, a.fetch_cmd,
+                        a.write_cmd, a.out_dir)
+
+
 def main():
+    if any(a in ("--reduce-trace", "--reduce-counters") for a in sys.argv[1:]):
+        reduce_main(sys.argv[1:])
+        return
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
@@ -952,6 +1365,8 @@ def main():
                     help="time the precompute of the f-gram rows by the f-gram model")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="also run a plain device copy of MIB MiB (counter calibration)")
+    ap.add_argument("--plan-out", metavar="FILE",
+                    help="write the run's library dispatches by phase (for the reducers)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -980,6 +1395,10 @@ def main():
         result = run_decode(args, cfg)
     else:
         result = run_prefill(args, cfg)
+    if args.plan_out:
+        json.dump({"config": cfg.name, "workload": describe(cfg), "steps": args.steps,
+                   "warmup": args.warmup, "copy_calibration_mib": args.copy_calibration,
+                   "argv": sys.argv, "entries": PLAN.entries}, open(args.plan_out, "w"))
     print(json.dumps(result), flush=True)
 
 

@@ -26,8 +26,8 @@
  *  - No call allocates device memory except scone_build_fgram_table,
  *    scone_host_alloc and the synchronous offline calls
  *    scone_discover_fgrams (when given no workspace) and
- *    scone_fgram_model_forward (and a 4-byte error word per device on first
- *    use).
+ *    scone_fgram_model_forward.  The device error word is a variable of the
+ *    library's own code object (one per GPU), not an allocation.
  *  - All buffers are owned by the caller except the table handle, which the
  *    library owns until scone_table_destroy.
  */
@@ -398,9 +398,12 @@ int scone_check(void* stream);
  * must make sure no lookup that reads it is still running. */
 void scone_table_destroy(scone_table_t* table);
 
-/* Properties of a built table; any output pointer may be NULL. */
+/* Properties of a built table; any output pointer may be NULL.  n: f-grams
+ * stored; capacity: slots; max_len: K; slot_bytes: 16 or 32; entries: slots
+ * in use, the f-grams plus the flagged suffix markers (so entries / capacity
+ * is the table's load). */
 int scone_table_info(const scone_table_t* table, int64_t* n, int64_t* capacity,
-                     int32_t* max_len, int32_t* slot_bytes);
+                     int32_t* max_len, int32_t* slot_bytes, int64_t* entries);
 
 /* A static, human-readable description of a status code. */
 const char* scone_strerror(int code);

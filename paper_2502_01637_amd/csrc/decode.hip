@@ -161,6 +161,24 @@ extern "C" int scone_decode_step(const scone_table_t* table, int32_t* ctx, int32
     if (S == 0) return SCONE_OK;
     if (!ctx_len || !new_tok || !out || (!ctx && ctx_cap > 0) || (!rows && n_rows > 0))
         return SCONE_EINVAL;
+    // Each wavefront rewrites its own sequence's context in place; the other
+    // outputs must not alias any input or each other.
+    {
+        const void* outs[3] = {out, fgram_ids, match_len};
+        const int64_t outs_b[3] = {S * row_bytes, span_bytes(S, 4), S};
+        const void* ins[4] = {ctx, ctx_len, new_tok, rows};
+        const int64_t ins_b[4] = {span_bytes(S, 4 * (int64_t)ctx_cap), span_bytes(S, 4),
+                                  span_bytes(S, 4), span_bytes(n_rows, row_bytes)};
+        for (int i = 0; i < 3; ++i) {
+            for (int j = 0; j < 4; ++j)
+                if (overlaps(outs[i], outs_b[i], ins[j], ins_b[j])) return SCONE_EINVAL;
+            for (int j = i + 1; j < 3; ++j)
+                if (overlaps(outs[i], outs_b[i], outs[j], outs_b[j])) return SCONE_EINVAL;
+        }
+        if (overlaps(ctx, ins_b[0], ctx_len, ins_b[1]) || overlaps(ctx, ins_b[0], new_tok, ins_b[2]) ||
+            overlaps(ctx_len, ins_b[1], new_tok, ins_b[2]))
+            return SCONE_EINVAL;
+    }
     int dev = 0;
     SCONE_HIP_TRY(hipGetDevice(&dev));
     if (dev != table->device) return SCONE_EINVAL;
@@ -180,5 +198,5 @@ extern "C" int scone_decode_step(const scone_table_t* table, int32_t* ctx, int32
                                            n_rows, row_bytes, 0, out, fgram_ids, match_len, err,
                                            st);
     }
-    return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
+    return status_of(e);
 }

@@ -180,6 +180,18 @@ extern "C" int scone_embed(const scone_table_t* table, const int32_t* token_ids,
     if (B * T > ((int64_t)1 << 62) / row_bytes) return SCONE_EINVAL;
     if (B * T == 0) return SCONE_OK;
     if (!token_ids || !out || (!rows && n_rows > 0)) return SCONE_EINVAL;
+    {
+        const int64_t n = B * T, out_b = n * row_bytes;
+        const void* outs[3] = {out, fgram_ids, match_len};
+        const int64_t outs_b[3] = {out_b, span_bytes(n, 4), n};
+        for (int i = 0; i < 3; ++i) {
+            if (overlaps(outs[i], outs_b[i], token_ids, span_bytes(n, 4)) ||
+                overlaps(outs[i], outs_b[i], rows, span_bytes(n_rows, row_bytes)))
+                return SCONE_EINVAL;
+            for (int j = i + 1; j < 3; ++j)
+                if (overlaps(outs[i], outs_b[i], outs[j], outs_b[j])) return SCONE_EINVAL;
+        }
+    }
     int dev = 0;
     SCONE_HIP_TRY(hipGetDevice(&dev));
     if (dev != table->device) return SCONE_EINVAL;
@@ -193,8 +205,7 @@ extern "C" int scone_embed(const scone_table_t* table, const int32_t* token_ids,
         if (fgram_ids || match_len)
             e0 = launch_lookup(table, token_ids, B, T, eff, fgram_ids, match_len, err, st);
         if (e0 == hipSuccess) e0 = launch_zero_rows(out, B * T * row_bytes, err, st);
-        if (e0 == hipErrorInvalidConfiguration) return SCONE_EINVAL;
-        return e0 == hipSuccess ? SCONE_OK : SCONE_EHIP;
+        return status_of(e0);
     }
     const uintptr_t align = (uintptr_t)rows | (uintptr_t)out | (uintptr_t)row_bytes;
     hipError_t e;
@@ -208,6 +219,5 @@ extern "C" int scone_embed(const scone_table_t* table, const int32_t* token_ids,
         e = dispatch_slots<uint8_t, false>(table, token_ids, B, T, eff, rows, n_rows, row_bytes,
                                            0, out, fgram_ids, match_len, err, st);
     }
-    if (e == hipErrorInvalidConfiguration) return SCONE_EINVAL;
-    return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
+    return status_of(e);
 }

@@ -2,7 +2,8 @@
 //
 // The embedding fetch is a pure memory copy (Section 1), so the kernel is an
 // HBM-bound streaming copy whose source rows are chosen by the ids.  Rows of
-// 1, 2, 4 or 8 KiB (16-byte aligned) take one wavefront per row.  Any other
+// 1 or 2 KiB (16-byte aligned) take one wavefront per row, rows of 4 or 8 KiB
+// one wavefront per KiB (gather_row_waves).  Any other
 // width views the output as a flat array of V-sized units (16 bytes when the
 // row width and the pointers allow).  Consecutive lanes own consecutive units, so
 // one wavefront reads 64 * 16 B = 1 KiB of one row per instruction and writes
@@ -72,16 +73,19 @@ __global__ __launch_bounds__(kGatherThreads) void k_gather(
     if (bad) atomicOr(err, err_bit(SCONE_EROW));
 }
 
-// Rows of 64*U 16-byte units (1, 2, 4 or 8 KiB): one wavefront per row, four
-// rows per workgroup.
+// Rows of 64*U 16-byte units (1, 2, 4 or 8 KiB): W = gather_row_waves(U) wavefronts
+// per row, each copying one W-th of it; consecutive wavefronts of a workgroup
+// take consecutive parts.
 template <int U>
 __global__ __launch_bounds__(kGatherThreads) void k_gather_rows(
     const int32_t* __restrict__ ids, int64_t n_tok, const u32x4* __restrict__ rows,
     int64_t n_rows, u32x4* __restrict__ out, unsigned* __restrict__ err, int64_t block0) {
-    const int64_t r = block_index(block0) * (kGatherThreads / 64) +
+    constexpr int W = gather_row_waves(U);
+    const int64_t w = block_index(block0) * (kGatherThreads / 64) +
                       __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t r = w / W;
     if (r >= n_tok) return;  // wave-uniform
-    copy_row_wave<U>(ids, r, rows, n_rows, out, err);
+    copy_row_part<U, W>(ids, r, (int)(w - r * W), rows, n_rows, out, err);
 }
 
 // Every id is out of range when the table has no rows: zero the output.
@@ -138,7 +142,8 @@ hipError_t launch_gather_any(const int32_t* ids, int64_t n_tok, const void* rows
     const int64_t upr16 = row_bytes / 16;
     if ((align & 15) == 0 && n_rows > 0 &&
         (upr16 == 64 || upr16 == 128 || upr16 == 256 || upr16 == 512)) {
-        const int64_t blocks = (n_tok + kGatherThreads / 64 - 1) / (kGatherThreads / 64);
+        const int64_t waves = n_tok * gather_row_waves((int)upr16 / 64);
+        const int64_t blocks = (waves + kGatherThreads / 64 - 1) / (kGatherThreads / 64);
         const u32x4* R = static_cast<const u32x4*>(rows);
         u32x4* O = static_cast<u32x4*>(out);
         return launch_blocks(blocks, kGatherThreads, [&](int64_t b0, dim3 grid) {
@@ -173,10 +178,14 @@ extern "C" int scone_gather(const int32_t* fgram_ids, int64_t n_tok, const void*
     if (n_tok > ((int64_t)1 << 62) / row_bytes) return SCONE_EINVAL;
     if (n_tok == 0) return SCONE_OK;
     if (!fgram_ids || !out || (!rows && n_rows > 0)) return SCONE_EINVAL;
+    // Rows are written while other wavefronts still read their ids and rows.
+    const int64_t out_b = n_tok * row_bytes;
+    if (overlaps(out, out_b, fgram_ids, span_bytes(n_tok, 4)) ||
+        overlaps(out, out_b, rows, span_bytes(n_rows, row_bytes)))
+        return SCONE_EINVAL;
     unsigned* err = device_error_word();
     if (!err) return SCONE_EHIP;
     const hipError_t e = launch_gather_any(fgram_ids, n_tok, rows, n_rows, row_bytes, out, err,
                                            static_cast<hipStream_t>(stream));
-    if (e == hipErrorInvalidConfiguration) return SCONE_EINVAL;
-    return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
+    return status_of(e);
 }

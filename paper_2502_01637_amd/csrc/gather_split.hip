@@ -219,5 +219,5 @@ extern "C" int scone_gather_split(const int32_t* fgram_ids, int64_t n_tok, const
                                static_cast<const u32x4*>(near_rows), n_near, n_far, keys, index,
                                mask, staging, upr, static_cast<u32x4*>(out), err, b0);
         });
-    return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
+    return status_of(e);
 }

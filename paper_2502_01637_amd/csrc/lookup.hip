@@ -77,6 +77,12 @@ extern "C" int scone_lookup(const scone_table_t* table, const int32_t* token_ids
     if (B > 0 && T > ((int64_t)1 << 62) / B) return SCONE_EINVAL;
     if (B * T == 0) return SCONE_OK;
     if (!token_ids || !fgram_ids) return SCONE_EINVAL;
+    // Workgroups read their tile's tokens plus a halo that other workgroups'
+    // positions own, so the outputs must not alias the tokens.
+    if (overlaps(fgram_ids, span_bytes(B * T, 4), token_ids, span_bytes(B * T, 4)) ||
+        overlaps(match_len, B * T, token_ids, span_bytes(B * T, 4)) ||
+        overlaps(match_len, B * T, fgram_ids, span_bytes(B * T, 4)))
+        return SCONE_EINVAL;
     int dev = 0;
     SCONE_HIP_TRY(hipGetDevice(&dev));
     if (dev != table->device) return SCONE_EINVAL;
@@ -85,8 +91,7 @@ extern "C" int scone_lookup(const scone_table_t* table, const int32_t* token_ids
     const int eff = max_n < table->max_len ? max_n : table->max_len;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const hipError_t e = launch_lookup(table, token_ids, B, T, eff, fgram_ids, match_len, err, st);
-    if (e == hipErrorInvalidConfiguration) return SCONE_EINVAL;
-    return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
+    return status_of(e);
 }
 
 // Pre-scan tagging: the lookup's match lengths and their histogram, without ids.
@@ -98,6 +103,10 @@ extern "C" int scone_tag(const scone_table_t* table, const int32_t* token_ids, i
     if (B > 0 && T > ((int64_t)1 << 62) / B) return SCONE_EINVAL;
     if (B * T == 0) return SCONE_OK;
     if (!token_ids || (!match_len && !hist)) return SCONE_EINVAL;
+    if (overlaps(match_len, B * T, token_ids, span_bytes(B * T, 4)) ||
+        overlaps(hist, 8 * (SCONE_MAX_FGRAM_LEN + 1), token_ids, span_bytes(B * T, 4)) ||
+        overlaps(hist, 8 * (SCONE_MAX_FGRAM_LEN + 1), match_len, B * T))
+        return SCONE_EINVAL;
     int dev = 0;
     SCONE_HIP_TRY(hipGetDevice(&dev));
     if (dev != table->device) return SCONE_EINVAL;
@@ -107,6 +116,5 @@ extern "C" int scone_tag(const scone_table_t* table, const int32_t* token_ids, i
     const hipError_t e = launch_lookup(table, token_ids, B, T, eff, nullptr, match_len, err,
                                        static_cast<hipStream_t>(stream),
                                        reinterpret_cast<unsigned long long*>(hist));
-    if (e == hipErrorInvalidConfiguration) return SCONE_EINVAL;
-    return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
+    return status_of(e);
 }

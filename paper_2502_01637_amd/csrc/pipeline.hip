@@ -32,10 +32,12 @@ __global__ __launch_bounds__(kTileThreads) void k_pipelined(
                             next_len, err);
         return;
     }
-    const int64_t r = (blk - n_lookup_blocks) * (kTileThreads / 64) +
+    constexpr int W = pipelined_row_waves(U);
+    const int64_t w = (blk - n_lookup_blocks) * (kTileThreads / 64) +
                       __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t r = w / W;
     if (r >= n_cur) return;  // wave-uniform
-    copy_row_wave<U>(cur_ids, r, rows, n_rows, out, err);
+    copy_row_part<U, W>(cur_ids, r, (int)(w - r * W), rows, n_rows, out, err);
 }
 
 struct Step {
@@ -60,7 +62,8 @@ hipError_t launch(const Step& s) {
     constexpr int P = TileShape<G>::kPositions;
     const int64_t tiles = (s.T + P - 1) / P;
     const int64_t n_lookup = s.B * tiles;
-    const int64_t n_gather = (s.n_cur + kTileThreads / 64 - 1) / (kTileThreads / 64);
+    const int64_t n_waves = s.n_cur * pipelined_row_waves(U);
+    const int64_t n_gather = (n_waves + kTileThreads / 64 - 1) / (kTileThreads / 64);
     return launch_blocks(n_lookup + n_gather, kTileThreads, [&](int64_t b0, dim3 grid) {
         hipLaunchKernelGGL((k_pipelined<SB, G, U>), grid, dim3(kTileThreads), 0, s.st,
                            static_cast<const Slot*>(s.tb->slots), (uint64_t)s.tb->capacity - 1,
@@ -86,12 +89,6 @@ hipError_t by_lanes(const Step& s, int units) {
                                         : by_units<SB, 2>(s, units);
 }
 
-bool overlaps(const void* a, int64_t a_bytes, const void* b, int64_t b_bytes) {
-    if (!a || !b || a_bytes == 0 || b_bytes == 0) return false;
-    const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
-    return pa < pb + (uintptr_t)b_bytes && pb < pa + (uintptr_t)a_bytes;
-}
-
 }  // namespace
 }  // namespace scone
 
@@ -109,12 +106,22 @@ extern "C" int scone_embed_pipelined(const scone_table_t* table, const int32_t* 
     const int64_t n_next = B * T;
     if (n_next > 0 && (!next_tokens || !next_ids)) return SCONE_EINVAL;
     if (n_cur > 0 && (!cur_ids || !out || (!rows && n_rows > 0))) return SCONE_EINVAL;
-    // The lookup writes while the gather reads: the next batch's outputs must
-    // not share memory with the current batch's ids.
-    if (n_next > 0 && n_cur > 0 &&
-        (overlaps(next_ids, n_next * 4, cur_ids, n_cur * 4) ||
-         overlaps(next_len, n_next, cur_ids, n_cur * 4)))
-        return SCONE_EINVAL;
+    // One launch writes next_ids, next_len and out while other workgroups of it
+    // read next_tokens (each tile with its halo) and cur_ids: no output may
+    // share memory with an input or with another output.
+    {
+        const int64_t tok_b = span_bytes(n_next, 4), len_b = n_next > 0 ? n_next : 0;
+        const int64_t cur_b = span_bytes(n_cur, 4), out_b = span_bytes(n_cur, row_bytes);
+        const void* outs[3] = {next_ids, next_len, n_cur > 0 ? out : nullptr};
+        const int64_t outs_b[3] = {tok_b, next_len ? len_b : 0, out_b};
+        for (int i = 0; i < 3; ++i) {
+            if (overlaps(outs[i], outs_b[i], next_tokens, tok_b) ||
+                overlaps(outs[i], outs_b[i], cur_ids, cur_b))
+                return SCONE_EINVAL;
+            for (int j = i + 1; j < 3; ++j)
+                if (overlaps(outs[i], outs_b[i], outs[j], outs_b[j])) return SCONE_EINVAL;
+        }
+    }
     int dev = 0;
     SCONE_HIP_TRY(hipGetDevice(&dev));
     if (dev != table->device) return SCONE_EINVAL;
@@ -138,6 +145,5 @@ extern "C" int scone_embed_pipelined(const scone_table_t* table, const int32_t* 
         if (e == hipSuccess && n_cur > 0)
             e = launch_gather_any(cur_ids, n_cur, rows, n_rows, row_bytes, out, err, st);
     }
-    if (e == hipErrorInvalidConfiguration) return SCONE_EINVAL;
-    return e == hipSuccess ? SCONE_OK : SCONE_EHIP;
+    return status_of(e);
 }

@@ -9,6 +9,10 @@ namespace {
 constexpr int kMaxDevices = 64;
 std::mutex g_mu;
 unsigned* g_err_word[kMaxDevices] = {};
+// The error word lives in the library's own device data (one copy per GPU,
+// zero when the code object loads), so raising and checking errors never
+// allocates.  Host code reaches it only through hipGetSymbolAddress.
+__device__ unsigned g_err_bits;
 }  // namespace
 
 int code_from_bits(unsigned word) {
@@ -22,13 +26,12 @@ unsigned* device_error_word() {
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
     std::lock_guard<std::mutex> lk(g_mu);
     if (!g_err_word[dev]) {
-        unsigned* p = nullptr;
-        if (hipMalloc(&p, sizeof(unsigned)) != hipSuccess) return nullptr;
-        if (hipMemset(p, 0, sizeof(unsigned)) != hipSuccess) {
-            (void)hipFree(p);
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(g_err_bits)) != hipSuccess || !p) {
+            (void)hipGetLastError();
             return nullptr;
         }
-        g_err_word[dev] = p;
+        g_err_word[dev] = static_cast<unsigned*>(p);
     }
     return g_err_word[dev];
 }
@@ -111,12 +114,13 @@ void scone_table_destroy(scone_table_t* t) {
 }
 
 int scone_table_info(const scone_table_t* t, int64_t* n, int64_t* capacity, int32_t* max_len,
-                     int32_t* slot_bytes) {
+                     int32_t* slot_bytes, int64_t* entries) {
     if (!t) return SCONE_EINVAL;
     if (n) *n = t->n;
     if (capacity) *capacity = t->capacity;
     if (max_len) *max_len = t->max_len;
     if (slot_bytes) *slot_bytes = t->slot_bytes;
+    if (entries) *entries = t->entries;
     return SCONE_OK;
 }
 

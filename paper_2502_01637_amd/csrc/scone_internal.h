@@ -15,14 +15,36 @@ __host__ __device__ constexpr unsigned err_bit(int code) { return 1u << code; }
 // Lowest status code whose bit is set in `word` (SCONE_OK for 0).
 int code_from_bits(unsigned word);
 
-// The current device's 4-byte error word (allocated on first use), or null if
-// the allocation failed.
+// The current device's 4-byte error word (a device variable of the library,
+// looked up once per device), or null if the lookup failed.
 unsigned* device_error_word();
 
 #define SCONE_HIP_TRY(expr)                                \
     do {                                                   \
         if ((expr) != hipSuccess) return SCONE_EHIP;       \
     } while (0)
+
+// Status of a sequence of launches: a grid the device cannot run is an
+// argument error; any other runtime failure is SCONE_EHIP.
+inline int status_of(hipError_t e) {
+    return e == hipSuccess ? SCONE_OK
+           : e == hipErrorInvalidConfiguration ? SCONE_EINVAL : SCONE_EHIP;
+}
+
+// n * size in bytes, saturated at 2^62 (sizes are validated against that bound).
+inline int64_t span_bytes(int64_t n, int64_t size) {
+    if (n <= 0 || size <= 0) return 0;
+    return n > ((int64_t)1 << 62) / size ? ((int64_t)1 << 62) : n * size;
+}
+
+// True when the byte ranges [a, a + a_bytes) and [b, b + b_bytes) share a
+// byte; a null pointer or an empty range shares nothing.  Used to reject
+// outputs that alias inputs a concurrent workgroup still reads.
+inline bool overlaps(const void* a, int64_t a_bytes, const void* b, int64_t b_bytes) {
+    if (!a || !b || a_bytes <= 0 || b_bytes <= 0) return false;
+    const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
+    return pa < pb + (uintptr_t)b_bytes && pb < pa + (uintptr_t)a_bytes;
+}
 
 // ------------------------------------------------------------- launches ----
 // A dispatch states its grid as a count of work-items held in 32 bits per
@@ -257,5 +279,6 @@ struct scone_table {
     int32_t slot_bytes; // 16 or 32
     int64_t n;          // f-grams stored
     int64_t capacity;   // slots, a power of two
+    int64_t entries;    // slots in use: the f-grams plus their suffix markers
     void* slots;        // device memory, capacity * slot_bytes
 };

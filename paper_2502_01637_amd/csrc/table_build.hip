@@ -122,6 +122,30 @@ __global__ __launch_bounds__(kBuildThreads) void k_count_long(
         atomicAdd(counts + threadIdx.x, (unsigned long long)s_c[threadIdx.x]);
 }
 
+// Counts the slots in use (f-grams and suffix markers, non-zero first key
+// word) after a build: kUsedPer slots per thread, one global add per workgroup.
+constexpr int kUsedPer = 16;
+
+template <int SB>
+__global__ __launch_bounds__(kBuildThreads) void k_count_used(
+    const typename SlotOps<SB>::Slot* __restrict__ slots, int64_t cap,
+    unsigned long long* __restrict__ used, int64_t block0) {
+    __shared__ unsigned s_c;
+    if (threadIdx.x == 0) s_c = 0;
+    __syncthreads();
+    const int64_t base = block_index(block0) * (kBuildThreads * kUsedPer) + threadIdx.x;
+    unsigned c = 0;
+#pragma unroll
+    for (int i = 0; i < kUsedPer; ++i) {
+        const int64_t k = base + (int64_t)i * kBuildThreads;
+        if (k < cap && slots[k].w0 != 0) ++c;
+    }
+    for (int off = 32; off > 0; off >>= 1) c += __shfl_down(c, off);
+    if ((threadIdx.x & 63) == 0 && c) atomicAdd(&s_c, c);
+    __syncthreads();
+    if (threadIdx.x == 0 && s_c) atomicAdd(used, (unsigned long long)s_c);
+}
+
 // Gives the entry of `key` kExtBit, inserting a marker when the key has no
 // entry.  A marker slot is claimed in three steps: its first key word goes
 // from 0 to kBusy (no key has length field 15), the rest of the key and the
@@ -231,10 +255,12 @@ extern "C" int scone_build_fgram_table(const int32_t* fgrams, const int32_t* len
     SCONE_HIP_TRY(hipGetDevice(&dev));
 
     void* slots = nullptr;
-    // status word at offset 0, counts of f-grams of length >= 4 and >= 6 at 8, 16
+    // status word at offset 0, counts of f-grams of length >= 4 and >= 6 at 8,
+    // 16, slots in use after the build at 24
     void* aux = nullptr;
     int64_t* slot_of = nullptr;
     int rc = SCONE_OK;
+    unsigned long long haux[4] = {0, 0, 0, 0};
     unsigned hstatus = 0;
     unsigned long long hcount[2] = {0, 0};
     uint64_t cap = 64;
@@ -292,11 +318,26 @@ extern "C" int scone_build_fgram_table(const int32_t* fgrams, const int32_t* len
             goto fail;
         }
     }
-    if (hipMemcpyAsync(&hstatus, status, sizeof(unsigned), hipMemcpyDeviceToHost, st) !=
-            hipSuccess ||
-        hipStreamSynchronize(st) != hipSuccess) {
-        rc = SCONE_EHIP;
-        goto fail;
+    {
+        unsigned long long* used =
+            reinterpret_cast<unsigned long long*>(static_cast<uint8_t*>(aux) + 24);
+        const int64_t per = (int64_t)kBuildThreads * kUsedPer;
+        const hipError_t e = launch_blocks(((int64_t)cap + per - 1) / per, kBuildThreads,
+                                           [&](int64_t b0, dim3 grid) {
+            if (slot_bytes == 16)
+                hipLaunchKernelGGL(k_count_used<16>, grid, dim3(kBuildThreads), 0, st,
+                                   static_cast<const Slot16*>(slots), (int64_t)cap, used, b0);
+            else
+                hipLaunchKernelGGL(k_count_used<32>, grid, dim3(kBuildThreads), 0, st,
+                                   static_cast<const Slot32*>(slots), (int64_t)cap, used, b0);
+        });
+        if (e != hipSuccess ||
+            hipMemcpyAsync(haux, aux, sizeof(haux), hipMemcpyDeviceToHost, st) != hipSuccess ||
+            hipStreamSynchronize(st) != hipSuccess) {
+            rc = SCONE_EHIP;
+            goto fail;
+        }
+        hstatus = (unsigned)(haux[0] & 0xffffffffu);
     }
     if (hstatus) {
         // Report argument-like data errors before structural ones.
@@ -322,6 +363,7 @@ extern "C" int scone_build_fgram_table(const int32_t* fgrams, const int32_t* len
         t->slot_bytes = slot_bytes;
         t->n = n;
         t->capacity = (int64_t)cap;
+        t->entries = (int64_t)haux[3];
         t->slots = slots;
         *out = t;
     }

@@ -107,7 +107,7 @@ int main(int argc, char** argv) {
     CHECK(scone_build_fgram_table(d_fg, d_len, d_ids, n, (int32_t)K, 0.5, stream, &table));
     int64_t stored = 0, capacity = 0;
     int32_t klen = 0, slot_bytes = 0;
-    CHECK(scone_table_info(table, &stored, &capacity, &klen, &slot_bytes));
+    CHECK(scone_table_info(table, &stored, &capacity, &klen, &slot_bytes, NULL));
     CHECK(scone_lookup(table, d_tok, B, T, (int32_t)max_n, d_fid, d_ml, stream));
     CHECK(scone_gather(d_fid, (int64_t)n_tok, d_rows, n_rows, row_bytes, d_out, SCONE_PLACE_HBM,
                        stream));

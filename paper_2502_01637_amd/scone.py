@@ -76,7 +76,8 @@ def _declare(L):
     L.scone_table_destroy.argtypes = [P]
     L.scone_table_destroy.restype = None
     L.scone_table_info.argtypes = [P, ctypes.POINTER(I64), ctypes.POINTER(I64),
-                                   ctypes.POINTER(I32), ctypes.POINTER(I32)]
+                                   ctypes.POINTER(I32), ctypes.POINTER(I32),
+                                   ctypes.POINTER(I64)]
     L.scone_table_info.restype = I
     L.scone_strerror.argtypes = [I]
     L.scone_strerror.restype = ctypes.c_char_p
@@ -128,11 +129,12 @@ class Table:
     def __init__(self, handle: ctypes.c_void_p, device: torch.device):
         self._h = handle
         self.device = device
-        n, cap = ctypes.c_int64(), ctypes.c_int64()
+        n, cap, ent = ctypes.c_int64(), ctypes.c_int64(), ctypes.c_int64()
         ml, sb = ctypes.c_int32(), ctypes.c_int32()
         _check(lib().scone_table_info(handle, ctypes.byref(n), ctypes.byref(cap),
-                                      ctypes.byref(ml), ctypes.byref(sb)), "scone_table_info")
-        self.n, self.capacity = n.value, cap.value
+                                      ctypes.byref(ml), ctypes.byref(sb), ctypes.byref(ent)),
+               "scone_table_info")
+        self.n, self.capacity, self.entries = n.value, cap.value, ent.value
         self.max_len, self.slot_bytes = ml.value, sb.value
 
     @property

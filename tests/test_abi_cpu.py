@@ -73,7 +73,7 @@ def test_host_side_argument_errors():
     # host memory and table bookkeeping
     assert L.scone_host_alloc(0, ctypes.byref(h), ctypes.byref(h)) == E
     assert L.scone_host_free(None) == S.scone.OK
-    assert L.scone_table_info(None, None, None, None, None) == E
+    assert L.scone_table_info(None, None, None, None, None, None) == E
     L.scone_table_destroy(None)
 
 
@@ -117,3 +117,85 @@ def test_fgram_model_layout_and_argument_errors():
                                        None, 10, None) == E
     assert L.scone_fgram_model_forward(None, None, None, 0, 3, None, 10, None, 512, 8, 1024, 1,
                                        None, 10, None) == S.scone.OK
+
+
+def _fake(base: int):
+    """A fake device address: the calls below reject aliasing before any
+    device access, so no memory is behind it."""
+    return ctypes.c_void_p(base)
+
+
+def test_aliasing_outputs_are_rejected_before_any_device_work():
+    """Outputs that share memory with an input (or another output) that other
+    workgroups of the same launch still read are argument errors.  A call
+    whose buffers do not alias gets past these checks and only then fails
+    here, at its first HIP call (SCONE_EHIP: no GPU in this process)."""
+    L = S.scone.lib()
+    E, H = S.scone.EINVAL, S.scone.EHIP
+    tbl = ctypes.create_string_buffer(64)          # stands in for a table handle
+    B, T, R = 4, 256, 4096
+    n = B * T
+    tok, ids, ln = _fake(1 << 32), _fake(2 << 32), _fake(3 << 32)
+    out, rows, cur = _fake(4 << 32), _fake(5 << 32), _fake(6 << 32)
+    # scone_lookup: ids or lengths over the tokens, lengths over the ids
+    assert L.scone_lookup(tbl, tok, B, T, 3, _fake((1 << 32) + 4 * n - 4), None, None) == E
+    assert L.scone_lookup(tbl, tok, B, T, 3, ids, _fake((1 << 32) + 8), None) == E
+    assert L.scone_lookup(tbl, tok, B, T, 3, ids, _fake((2 << 32) + 4 * n - 1), None) == E
+    assert L.scone_lookup(tbl, tok, B, T, 3, ids, ln, None) == H
+    # scone_tag: lengths over the tokens
+    assert L.scone_tag(tbl, tok, B, T, 3, _fake(1 << 32), None, None) == E
+    # scone_gather: output over the ids or over the row table
+    assert L.scone_gather(ids, n, rows, 100, R, _fake((2 << 32) - n * R + 1), 0, None) == E
+    assert L.scone_gather(ids, n, rows, 100, R, _fake((5 << 32) + 99 * R), 0, None) == E
+    assert L.scone_gather(ids, n, rows, 100, R, out, 0, None) == H
+    # scone_embed: output over tokens, ids over output, lengths over ids
+    assert L.scone_embed(tbl, tok, B, T, 3, rows, 100, R, 0, _fake(1 << 32), ids, ln,
+                         None) == E
+    assert L.scone_embed(tbl, tok, B, T, 3, rows, 100, R, 0, out, _fake((4 << 32) + 64), ln,
+                         None) == E
+    assert L.scone_embed(tbl, tok, B, T, 3, rows, 100, R, 0, out, ids, _fake(2 << 32),
+                         None) == E
+    assert L.scone_embed(tbl, tok, B, T, 3, rows, 100, R, 0, out, ids, ln, None) == H
+    # scone_embed_pipelined: every output against next_tokens, cur_ids and the
+    # other outputs
+    P = L.scone_embed_pipelined
+    assert P(tbl, tok, B, T, 3, ids, ln, cur, n, rows, 100, R, 0, out, None) == H
+    assert P(tbl, tok, B, T, 3, _fake(6 << 32), ln, cur, n, rows, 100, R, 0, out, None) == E
+    assert P(tbl, tok, B, T, 3, ids, _fake(6 << 32), cur, n, rows, 100, R, 0, out, None) == E
+    assert P(tbl, tok, B, T, 3, ids, ln, cur, n, rows, 100, R, 0, _fake(6 << 32), None) == E
+    assert P(tbl, tok, B, T, 3, ids, ln, cur, n, rows, 100, R, 0,
+             _fake((1 << 32) + 4 * n - 16), None) == E                      # out over tokens
+    assert P(tbl, tok, B, T, 3, _fake((1 << 32) + 4), ln, cur, n, rows, 100, R, 0, out,
+             None) == E                                                     # ids over tokens
+    assert P(tbl, tok, B, T, 3, ids, ln, cur, n, rows, 100, R, 0, _fake((2 << 32) + 4),
+             None) == E                                                     # out over next ids
+    assert P(tbl, tok, B, T, 3, ids, _fake((4 << 32) + 7), cur, n, rows, 100, R, 0, out,
+             None) == E                                                     # lengths over out
+    # scone_decode_step: outputs against the context, lengths, new tokens, rows
+    D = L.scone_decode_step
+    ctx, clen, newt = _fake(7 << 32), _fake(8 << 32), _fake(9 << 32)
+    assert D(tbl, ctx, clen, 4, newt, B, 3, rows, 100, R, 0, out, ids, ln, None) == H
+    assert D(tbl, ctx, clen, 4, newt, B, 3, rows, 100, R, 0, _fake(7 << 32), ids, ln,
+             None) == E
+    assert D(tbl, ctx, clen, 4, newt, B, 3, rows, 100, R, 0, out, _fake(9 << 32), ln,
+             None) == E
+    assert D(tbl, ctx, clen, 4, newt, B, 3, rows, 100, R, 0, out, ids, _fake(8 << 32),
+             None) == E
+    assert D(tbl, ctx, _fake(9 << 32), 4, newt, B, 3, rows, 100, R, 0, out, ids, ln,
+             None) == E
+
+
+def test_decode_host_argument_errors():
+    L = S.scone.lib()
+    E = S.scone.EINVAL
+    tbl = ctypes.create_string_buffer(64)
+    D = L.scone_decode_step
+    p = _fake(1 << 40)
+    assert D(None, p, p, 4, p, 1, 3, p, 10, 16, 0, p, None, None, None) == E     # no table
+    assert D(tbl, p, p, 4, p, -1, 3, p, 10, 16, 0, p, None, None, None) == E     # S < 0
+    assert D(tbl, p, p, 4, p, 1, 0, p, 10, 16, 0, p, None, None, None) == E      # max_n < 1
+    assert D(tbl, p, p, 4, p, 1, 3, p, 10, 0, 0, p, None, None, None) == E       # row_bytes
+    assert D(tbl, p, p, 4, p, 1, 3, p, 10, 16, 2, p, None, None, None) == E      # placement
+    assert D(tbl, p, p, 64, p, 1, 3, p, 10, 16, 0, p, None, None, None) == E     # ctx_cap > 63
+    assert D(tbl, p, None, 4, p, 1, 3, p, 10, 16, 0, p, None, None, None) == E   # no ctx_len
+    assert D(tbl, p, p, 4, p, 0, 3, p, 10, 16, 0, p, None, None, None) == S.scone.OK

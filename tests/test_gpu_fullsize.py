@@ -50,12 +50,17 @@ def sampled_oracle_rows(cfg, out, exp_ids, n=2048, seed=0):
     return got.numpy().tobytes() == exp.tobytes()
 
 
-@pytest.mark.parametrize("name", ["c2_1m", "c3_10m_k5"])
-def test_hbm_prefill_full_size(name):
+# 0.25 is the load target bench.py and the binding use (on c3: 2^26 slots
+# holding the f-grams and about 5M suffix markers); 0.5 halves the table.
+@pytest.mark.parametrize("name,max_load", [("c2_1m", 0.25), ("c2_1m", 0.5),
+                                           ("c3_10m_k5", 0.25), ("c3_10m_k5", 0.5)])
+def test_hbm_prefill_full_size(name, max_load):
     cfg = CONFIGS[name]
     w = make_workload(cfg)
     o = oracle.OracleTable(w.fgrams, w.lengths, w.ids)
-    tb = build_gpu(w.fgrams, w.lengths, w.ids, max_load=0.5)
+    tb = build_gpu(w.fgrams, w.lengths, w.ids, max_load=max_load)
+    assert tb.n == cfg.n_fgrams and tb.n <= tb.entries <= tb.capacity
+    assert tb.entries <= max_load * tb.capacity * 1.01
     E = device_rows(cfg)
     batches = query_batches(w, 2)
     expected = []
@@ -85,6 +90,21 @@ def test_hbm_prefill_full_size(name):
         np.testing.assert_array_equal(ids_buf[k].cpu().numpy(), expected[k])
         assert rows_match_generator(cfg, out, expected[k]), (name, "pipelined", k)
         assert sampled_oracle_rows(cfg, out, expected[k], seed=10 + k), (name, "pipelined", k)
+    del outs
+    # bench.py's no-reuse steps: the pipelined launch gathering uniform random
+    # ids over the whole table while it looks up a real batch
+    g = torch.Generator(device="cuda")
+    g.manual_seed(cfg.seed)
+    uids = torch.randint(0, cfg.n_rows, batches[0].shape, dtype=torch.int32, device="cuda",
+                         generator=g)
+    nxt = torch.empty_like(uids)
+    out_u = S.embed_pipelined(tb, Xd[1], cfg.max_n, nxt, uids, E)
+    S.check_ok()
+    np.testing.assert_array_equal(nxt.cpu().numpy(), expected[1])
+    assert rows_match_generator(cfg, out_u, uids.cpu().numpy()), (name, "no-reuse")
+    out_g = S.gather(uids, E)
+    S.check_ok()
+    assert torch.equal(out_g.view(torch.int16), out_u.view(torch.int16)), (name, "uniform")
 
 
 def test_host_pinned_full_size():

@@ -121,6 +121,24 @@ def test_load_factors(max_load):
     tb, _ = compare_lookup(w.fgrams, w.lengths, w.ids, w.tokens, 3, max_load=max_load)
     assert tb.n == 30_000 and tb.capacity >= 30_000 / max_load
     assert tb.capacity & (tb.capacity - 1) == 0
+    assert tb.entries == tb.n          # K = 3: no suffix markers
+
+
+def test_table_entries_count_suffix_markers():
+    """entries = the f-grams plus one marker per distinct length-3 suffix of an
+    f-gram of length >= 4 that is not itself an f-gram, plus the extra copies
+    that concurrent inserts of one marker may leave (at most one slot per long
+    f-gram in all; a few percent of the markers on this Zipf set, whose
+    frequent suffixes are shared by many f-grams)."""
+    cfg = scaled(CONFIGS["c3_10m_k5"], n_fgrams=40_000, B=2, T=100)
+    w = make_workload(cfg)
+    tb = build_gpu(w.fgrams, w.lengths, w.ids, max_load=0.25)
+    fgrams = {tuple(r[:L]) for r, L in zip(w.fgrams.tolist(), w.lengths.tolist())}
+    long_ = [tuple(r[L - 3:L]) for r, L in zip(w.fgrams.tolist(), w.lengths.tolist()) if L >= 4]
+    markers = {s for s in long_ if s not in fgrams}
+    assert tb.n == len(fgrams)
+    assert tb.n + len(markers) <= tb.entries <= tb.n + len(long_)
+    assert tb.entries <= tb.n + len(markers) + max(8, len(markers) // 10)
 
 
 def test_empty_inputs():
