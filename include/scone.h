@@ -52,7 +52,8 @@ enum scone_status {
     SCONE_ENOMEM = 6,  /* device or pinned host allocation failed */
     SCONE_EHIP = 7,    /* a HIP runtime call failed */
     SCONE_ETOKEN = 8,  /* a token outside [0, SCONE_TOKEN_LIMIT) */
-    SCONE_EROW = 9     /* a row id outside [0, n_rows) */
+    SCONE_EROW = 9,    /* a row id outside [0, n_rows) */
+    SCONE_ESCRATCH = 10 /* the call needs more than the library's fixed scratch buffer */
 };
 
 enum scone_placement {
@@ -272,6 +273,29 @@ int scone_gather_split(const int32_t* fgram_ids, int64_t n_tok, const void* near
 /* Bytes of workspace scone_gather_split needs for n_tok rows of row_bytes, or
  * -1 for invalid sizes (worst case: every id distinct and far). */
 int64_t scone_gather_split_workspace(int64_t n_tok, int64_t row_bytes);
+
+/* Size of the fixed scratch buffer of scone_gather_split_static (bytes, per GPU). */
+#define SCONE_SPLIT_STATIC_BYTES (32 << 20)
+
+/*
+ * scone_gather_split without a workspace argument and without any allocation,
+ * for callers that cannot allocate device memory: code being captured into a
+ * HIP graph, tight serving loops (a decoding step for a few hundred sequences
+ * with the f-gram rows in host memory), harnesses that forbid hipMalloc.
+ * Arguments, results and errors are those of scone_gather_split; the dedupe
+ * set and the staged rows live in a fixed buffer of SCONE_SPLIT_STATIC_BYTES
+ * in the library's own device data (one per GPU, held until the process
+ * ends).  A call whose scone_gather_split_workspace(n_tok, row_bytes) exceeds
+ * that size returns SCONE_ESCRATCH and launches nothing (for 4 KiB rows, up
+ * to about 8,100 tokens fit).  Every call on a GPU shares that GPU's buffer:
+ * calls on one stream run in order, but calls that can overlap (other
+ * streams, other threads) race and their results are unspecified.  Each call
+ * resets the parts it reads, so nothing carries over from the last call.
+ * Asynchronous on `stream`; launches kernels only.
+ */
+int scone_gather_split_static(const int32_t* fgram_ids, int64_t n_tok, const void* near_rows,
+                              int64_t n_near, const void* far_rows, int64_t n_far,
+                              int64_t row_bytes, void* out, int32_t* n_unique, void* stream);
 
 /*
  * F-gram discovery (Algorithm 3: count every n-gram, n = 2..max_len, of all

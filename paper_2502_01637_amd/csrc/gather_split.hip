@@ -14,6 +14,8 @@
 //   4. k_split_fetch  - copy each distinct far row from host memory into the
 //                       device staging area, one wavefront per row,
 //   5. k_split_gather - out[k] = near[id] or staged[index of id], from HBM.
+#include <mutex>
+
 #include "scone_internal.h"
 
 namespace scone {
@@ -163,21 +165,13 @@ extern "C" int64_t scone_gather_split_workspace(int64_t n_tok, int64_t row_bytes
     return scone::layout(n_tok, row_bytes).total;
 }
 
-extern "C" int scone_gather_split(const int32_t* fgram_ids, int64_t n_tok, const void* near_rows,
-                                  int64_t n_near, const void* far_rows, int64_t n_far,
-                                  int64_t row_bytes, void* out, void* workspace,
-                                  int64_t workspace_bytes, int32_t* n_unique, void* stream) {
-    using namespace scone;
-    if (n_tok < 0 || n_near < 0 || n_far < 0 || row_bytes <= 0) return SCONE_EINVAL;
-    if (row_bytes % 16 != 0 || ((uintptr_t)near_rows | (uintptr_t)far_rows | (uintptr_t)out |
-                                (uintptr_t)workspace) % 16 != 0)
-        return SCONE_EINVAL;
-    if (n_near + n_far > ((int64_t)1 << 31) || n_tok > ((int64_t)1 << 40) / row_bytes)
-        return SCONE_EINVAL;
-    if (n_tok == 0) return SCONE_OK;
-    if (!fgram_ids || !out || !workspace || (n_near > 0 && !near_rows) ||
-        (n_far > 0 && !far_rows))
-        return SCONE_EINVAL;
+namespace scone {
+namespace {
+
+// Everything of scone_gather_split after the workspace is known.
+int split_run(const int32_t* fgram_ids, int64_t n_tok, const void* near_rows, int64_t n_near,
+              const void* far_rows, int64_t n_far, int64_t row_bytes, void* out,
+              void* workspace, int64_t workspace_bytes, int32_t* n_unique, void* stream) {
     const Layout l = layout(n_tok, row_bytes);
     if (workspace_bytes < l.total) return SCONE_EINVAL;
     unsigned* err = device_error_word();
@@ -220,4 +214,89 @@ extern "C" int scone_gather_split(const int32_t* fgram_ids, int64_t n_tok, const
                                mask, staging, upr, static_cast<u32x4*>(out), err, b0);
         });
     return status_of(e);
+}
+
+// Argument checks shared by both entry points (the workspace is checked by
+// each); SCONE_OK means the call has work to do.
+int split_args(const int32_t* fgram_ids, int64_t n_tok, const void* near_rows, int64_t n_near,
+               const void* far_rows, int64_t n_far, int64_t row_bytes, const void* out) {
+    if (n_tok < 0 || n_near < 0 || n_far < 0 || row_bytes <= 0) return SCONE_EINVAL;
+    if (row_bytes % 16 != 0 ||
+        ((uintptr_t)near_rows | (uintptr_t)far_rows | (uintptr_t)out) % 16 != 0)
+        return SCONE_EINVAL;
+    if (n_near + n_far > ((int64_t)1 << 31) || n_tok > ((int64_t)1 << 40) / row_bytes)
+        return SCONE_EINVAL;
+    if (n_tok > 0 && (!fgram_ids || !out || (n_near > 0 && !near_rows) ||
+                      (n_far > 0 && !far_rows)))
+        return SCONE_EINVAL;
+    if (overlaps(out, n_tok * row_bytes, fgram_ids, span_bytes(n_tok, 4)) ||
+        overlaps(out, n_tok * row_bytes, near_rows, span_bytes(n_near, row_bytes)))
+        return SCONE_EINVAL;
+    return SCONE_OK;
+}
+
+}  // namespace
+}  // namespace scone
+
+extern "C" int scone_gather_split(const int32_t* fgram_ids, int64_t n_tok, const void* near_rows,
+                                  int64_t n_near, const void* far_rows, int64_t n_far,
+                                  int64_t row_bytes, void* out, void* workspace,
+                                  int64_t workspace_bytes, int32_t* n_unique, void* stream) {
+    using namespace scone;
+    const int rc = split_args(fgram_ids, n_tok, near_rows, n_near, far_rows, n_far, row_bytes,
+                              out);
+    if (rc != SCONE_OK) return rc;
+    if ((uintptr_t)workspace % 16 != 0) return SCONE_EINVAL;
+    if (n_tok == 0) return SCONE_OK;
+    if (!workspace) return SCONE_EINVAL;
+    return split_run(fgram_ids, n_tok, near_rows, n_near, far_rows, n_far, row_bytes, out,
+                     workspace, workspace_bytes, n_unique, stream);
+}
+
+namespace scone {
+namespace {
+
+// The scratch of scone_gather_split_static: a fixed buffer in the library's
+// own device data, one copy per GPU, held until the process ends.  Host code
+// never uses this name as an address: each device's copy is looked up once
+// with hipGetSymbolAddress and that pointer is passed to the kernels.
+static __device__ __align__(256) uint8_t scratch[SCONE_SPLIT_STATIC_BYTES];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxScratchDevices] = {};
+
+// This device's copy of `scratch`, or null if the lookup failed.
+void* device_scratch() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxScratchDevices) return nullptr;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        g_scratch[dev] = p;
+    }
+    return g_scratch[dev];
+}
+
+}  // namespace
+}  // namespace scone
+
+extern "C" int scone_gather_split_static(const int32_t* fgram_ids, int64_t n_tok,
+                                         const void* near_rows, int64_t n_near,
+                                         const void* far_rows, int64_t n_far, int64_t row_bytes,
+                                         void* out, int32_t* n_unique, void* stream) {
+    using namespace scone;
+    const int rc = split_args(fgram_ids, n_tok, near_rows, n_near, far_rows, n_far, row_bytes,
+                              out);
+    if (rc != SCONE_OK) return rc;
+    if (n_tok == 0) return SCONE_OK;
+    if (layout(n_tok, row_bytes).total > (int64_t)SCONE_SPLIT_STATIC_BYTES) return SCONE_ESCRATCH;
+    void* ws = device_scratch();
+    if (!ws) return SCONE_EHIP;
+    return split_run(fgram_ids, n_tok, near_rows, n_near, far_rows, n_far, row_bytes, out, ws,
+                     (int64_t)SCONE_SPLIT_STATIC_BYTES, n_unique, stream);
 }

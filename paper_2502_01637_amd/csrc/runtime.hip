@@ -74,6 +74,7 @@ const char* scone_strerror(int code) {
         case SCONE_EHIP: return "HIP runtime error";
         case SCONE_ETOKEN: return "token outside [0, 65536)";
         case SCONE_EROW: return "row id outside [0, n_rows)";
+        case SCONE_ESCRATCH: return "call exceeds the fixed scratch buffer";
         default: return "unknown status";
     }
 }

@@ -18,7 +18,8 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libscone.so")
 
-OK, EINVAL, ELEN, EID, EDUP, EFULL, ENOMEM, EHIP, ETOKEN, EROW = range(10)
+OK, EINVAL, ELEN, EID, EDUP, EFULL, ENOMEM, EHIP, ETOKEN, EROW, ESCRATCH = range(11)
+SPLIT_STATIC_BYTES = 32 << 20   # scone_gather_split_static's scratch (SCONE_SPLIT_STATIC_BYTES)
 PLACE_HBM, PLACE_HOST = 0, 1
 MAX_FGRAM_LEN = 7
 TOKEN_LIMIT = 65536
@@ -61,6 +62,8 @@ def _declare(L):
     L.scone_gather_split.restype = I
     L.scone_gather_split_workspace.argtypes = [I64, I64]
     L.scone_gather_split_workspace.restype = I64
+    L.scone_gather_split_static.argtypes = [P, I64, P, I64, P, I64, I64, P, P, P]
+    L.scone_gather_split_static.restype = I
     L.scone_fgram_model_forward.argtypes = [P, P, P, I64, I32, P, I64, P, I32, I32, I32, I32,
                                             P, I64, P]
     L.scone_fgram_model_forward.restype = I

@@ -29,8 +29,8 @@ def test_every_declared_symbol_is_exported():
 
 def test_status_strings():
     L = S.scone.lib()
-    for code in range(10):
-        assert L.scone_strerror(code)
+    for code in range(11):
+        assert L.scone_strerror(code) and L.scone_strerror(code) != b"unknown status"
     assert L.scone_strerror(S.scone.EROW) == b"row id outside [0, n_rows)"
     assert L.scone_strerror(1234) == b"unknown status"
 
@@ -199,3 +199,23 @@ def test_decode_host_argument_errors():
     assert D(tbl, p, p, 64, p, 1, 3, p, 10, 16, 0, p, None, None, None) == E     # ctx_cap > 63
     assert D(tbl, p, None, 4, p, 1, 3, p, 10, 16, 0, p, None, None, None) == E   # no ctx_len
     assert D(tbl, p, p, 4, p, 0, 3, p, 10, 16, 0, p, None, None, None) == S.scone.OK
+
+
+def test_static_split_gather_checks_its_scratch_limit_on_the_host():
+    """scone_gather_split_static refuses work beyond its fixed scratch before
+    any device work (SCONE_ESCRATCH) and checks arguments like
+    scone_gather_split; a call that fits gets past the checks and only then
+    fails here, at its first HIP call."""
+    L = S.scone.lib()
+    F = L.scone_gather_split_static
+    ids, near, far, out = _fake(1 << 32), _fake(2 << 32), _fake(3 << 32), _fake(4 << 32)
+    R = 4096
+    limit = S.scone.SPLIT_STATIC_BYTES
+    fits = max(n for n in range(1, 20000) if L.scone_gather_split_workspace(n, R) <= limit)
+    assert 7000 < fits < 8192
+    assert F(ids, fits + 1, near, 10, far, 10, R, out, None, None) == S.scone.ESCRATCH
+    assert F(ids, fits, near, 10, far, 10, R, out, None, None) == S.scone.EHIP
+    assert F(ids, 0, near, 10, far, 10, R, out, None, None) == S.scone.OK
+    assert F(ids, 5, near, 10, far, 10, 24, out, None, None) == S.scone.EINVAL   # width % 16
+    assert F(None, 5, near, 10, far, 10, R, out, None, None) == S.scone.EINVAL
+    assert F(ids, 5, near, 10, far, 10, R, _fake((1 << 32) + 8), None, None) == S.scone.EINVAL
