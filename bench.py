@@ -157,9 +157,13 @@ def split_placement(S, torch, cfg, table, rows, X, fid, outs, K, warmup):
     ws = torch.empty(S.split_workspace_bytes(cfg.n_tok, cfg.row_bytes), dtype=torch.uint8,
                      device=dev)
     nu = torch.zeros(1, dtype=torch.int32, device=dev)
+    SPLIT = ("k_split_clear", "k_split_insert", "k_split_number", "k_split_fetch",
+             "k_split_gather")
     for k in range(warmup):
         S.lookup(table, X[k % N_BATCHES], cfg.max_n, fgram_ids=fid)
         S.gather_split(fid, near, far, ws, out=outs[k % N_BATCHES], n_unique=nu)
+        for kern in ("k_lookup",) + SPLIT:
+            PLAN.add("split_warmup", kern)
     if S.check() != 0:
         raise SystemExit("device error in split-placement warm-up")
     ev, uniq = [], []
@@ -174,6 +178,8 @@ def split_placement(S, torch, cfg, table, rows, X, fid, outs, K, warmup):
         if e:
             e[0].record()
         S.gather_split(fid, near, far, ws, out=outs[k % N_BATCHES], n_unique=nu)
+        for kern in ("k_lookup",) + SPLIT:
+            PLAN.add("split_timed", kern)
         if e:
             e[1].record()
             uniq.append(nu.clone())
@@ -187,6 +193,8 @@ def split_placement(S, torch, cfg, table, rows, X, fid, outs, K, warmup):
     ids0, _ = S.lookup(table, X[0], cfg.max_n)
     a = S.gather(ids0, rows)
     b = S.gather_split(ids0, near, far, ws)
+    for kern in ("k_lookup", "k_gather") + SPLIT:
+        PLAN.add("split_parity", kern)
     same = bool(torch.equal(a.view(torch.int16), b.view(torch.int16)))
     del near, ws
     return {"tokens_per_s": cfg.n_tok * K / wall, "ms_per_step": wall * 1e3 / K,
@@ -661,12 +669,15 @@ def run_prefill(args, cfg):
         "traffic": None if traffic is None else traffic["traffic_bytes_per_launch"],
         "kernel": "scone_embed_pipelined (k_pipelined)",
         "algorithmic_bytes_per_launch": alg_bytes,
-        "cache_assisted": True,
-        "note": "frac counts algorithmic bytes over the step time on the Zipf workload, whose "
-                "repeated rows the L2s and the 256 MB last-level cache serve in part; "
-                "no_reuse is the same kernel over uniform random ids; traffic is L2-miss "
-                "bytes (FETCH_SIZE + WRITE_SIZE, calibrated), which include last-level-cache "
-                "hits: gfx950's counters do not separate DRAM from that cache",
+        "cache_assisted": not host,
+        "note": ("frac counts the row bytes read over PCIe (the host-pinned table is not "
+                 "cached on the device) over the step time; no_reuse is the same kernel over "
+                 "uniform random ids" if host else
+                 "frac counts algorithmic bytes over the step time on the Zipf workload, whose "
+                 "repeated rows the L2s and the 256 MB last-level cache serve in part; "
+                 "no_reuse is the same kernel over uniform random ids; traffic is L2-miss "
+                 "bytes (FETCH_SIZE + WRITE_SIZE, calibrated), which include last-level-cache "
+                 "hits: gfx950's counters do not separate DRAM from that cache"),
         "no_reuse": {"achieved": nr_rate, "frac": nr_rate / peak, "us": noreuse_ms * 1e3,
                      "traffic": None if traffic is None
                      else traffic.get("noreuse_traffic_bytes_per_launch"),
@@ -741,19 +752,20 @@ def run_decode(args, cfg):
     out = torch.empty((Sq, cfg.d), dtype=E.dtype, device=dev)
     torch.cuda.synchronize()
 
-    def run_all():
+    def run_all(phase):
         clen.fill_(0)
         for s in range(steps):
             S.decode_step(table, ctx, clen, Xs[s], cfg.max_n, E, out, fgram_ids=ids[s],
                           match_len=lens[s])
+        PLAN.add(phase, "k_decode", steps)
 
     # warm-up pass, then the timed eager pass (the host launches every step)
-    run_all()
+    run_all("decode_warmup")
     if S.check() != 0:
         raise SystemExit("device error in decode warm-up")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    run_all()
+    run_all("decode_eager")
     torch.cuda.synchronize()
     eager_wall = time.perf_counter() - t0
     if S.check() != 0:
@@ -779,6 +791,7 @@ def run_decode(args, cfg):
         g.replay()
         e1.record()
         torch.cuda.synchronize()
+        PLAN.add("decode_graph", "k_decode", steps)
         graph_times.append(time.perf_counter() - t0)
         graph_ev_ms.append(e0.elapsed_time(e1))
         if S.check() != 0:
@@ -818,6 +831,7 @@ def run_decode(args, cfg):
             gq.replay()
             e1.record()
             torch.cuda.synchronize()
+            PLAN.add(f"decode_sweep_{sq}", "k_decode", st_n)
             ev_ms.append(e0.elapsed_time(e1))
         if S.check() != 0 or not np.array_equal(ids_q.cpu().numpy(), ids_eager[:st_n, :sq]):
             raise SystemExit(f"batch-size sweep at {sq} sequences differs from the eager decode")
@@ -882,6 +896,7 @@ def run_decode(args, cfg):
         clen.fill_(0)
         g.replay()
         torch.cuda.synchronize()
+        PLAN.add("decode_parity", "k_decode", steps)
         result["cpu_baseline"] = {
             "value": passes * tokens / elapsed, "unit": "tokens/s", "cores": 1,
             "kind": "oracle",
@@ -1170,7 +1185,7 @@ def _read_csv(path):
         return list(csv.DictReader(f))
 
 
-def reduce_trace(trace_csv, plan_path, bench_json, out_md, profile_cmd):
+def reduce_trace(trace_csv, plan_path, bench_json, out_md, profile_cmd, bench_plain=False):
     """profiles/<workload>_kernel_trace.md from a --kernel-trace run."""
     import statistics as st
     plan = json.load(open(plan_path))
@@ -1190,7 +1205,8 @@ def reduce_trace(trace_csv, plan_path, bench_json, out_md, profile_cmd):
     med = lambda L: st.median(x["ns"] for x in L) / 1e3
     span = lambda L: f"{L[0]['Dispatch_Id']}-{L[-1]['Dispatch_Id']}"
     cfgname = plan["config"]
-    srcs = sorted({s for v in KERNEL_SOURCES.values() for s in v} | {"lookup.hip"})
+    srcs = sorted({s for v in KERNEL_SOURCES.values() for s in v}
+                  | {"lookup.hip", "decode.hip", "gather_split.hip", "runtime.hip"})
     L = [f"# Kernel trace: {cfgname} ({plan['workload']})\n",
          "Command (one MI355X, `<repo>` the repository root):\n", f"    {profile_cmd}\n",
          "Reduced with `python bench.py --reduce-trace <out>/run_kernel_trace.csv "
@@ -1204,30 +1220,39 @@ def reduce_trace(trace_csv, plan_path, bench_json, out_md, profile_cmd):
                  f"med_ns={st.median(ns):10.1f} min_ns={min(ns):9d} max_ns={max(ns):9d} "
                  f"grid={r0['Grid_Size_X']} wg={r0['Workgroup_Size_X']} vgpr={r0['VGPR_Count']} "
                  f"lds={r0['LDS_Block_Size']}")
-    L += ["```\n", f"By phase ({plan['steps']} timed steps each; dispatch numbers from the csv):\n",
-          "```"]
-    for phase in ("pipelined_timed", "noreuse_timed", "serial_timed", "fused_timed",
-                  "uniform_timed", "contiguous_timed", "cold_serial", "cold_pipelined"):
-        if phase not in ph:
+    L += ["```\n", "By phase (dispatch numbers from the csv; warm-up and parity launches "
+                    "left out):\n", "```"]
+    for phase, rs_all in ph.items():
+        if phase.endswith(("_warmup", "_first_lookup", "parity")):
             continue
         groups = {}
-        for r in ph[phase]:
+        for r in rs_all:
             groups.setdefault(_short(r["Kernel_Name"]), []).append(r)
         for name, rs in groups.items():
-            L.append(f"{phase:17s} {name[:40]:40s} n={len(rs):3d} (dispatches {span(rs)}) "
-                     f"mean {us(rs):8.2f} us  median {med(rs):8.2f} us")
+            L.append(f"{phase:17s} {name[:40]:40s} n={len(rs):5d} (dispatches {span(rs)}) "
+                     f"mean {us(rs):9.2f} us  median {med(rs):9.2f} us")
     L.append("```\n")
-    if bench:
-        L.append("bench.py's own figures in the same run (HIP events, under the profiler): "
+    where = ("a run of the same command without the profiler, in the same call" if bench_plain
+             else "HIP events in the same run, under the profiler")
+    if bench and "pipelined_us" in bench:
+        L.append(f"bench.py's own figures ({where}): "
                  f"pipelined step {bench['pipelined_us']:.1f} us (device time of the timed "
                  f"region per step), no-reuse pipelined step "
                  f"{bench['roofline']['no_reuse']['us']:.1f} us, serial lookup "
                  f"{bench['lookup_us']:.1f} us + gather {bench['gather_us']:.1f} us, "
                  f"uniform-id gather {bench['uniform_id_gather']['us']:.1f} us, contiguous "
                  f"rows {bench['sequential_row_gather']['us']:.1f} us; headline "
-                 f"{bench['value'] / 1e9:.3f} G tokens/s, roofline frac "
+                 f"{bench['value'] / 1e6:.1f} M tokens/s, roofline frac "
                  f"{bench['roofline']['frac']:.3f} (no reuse "
                  f"{bench['roofline']['no_reuse']['frac']:.3f}).\n")
+    elif bench and "graph_us_per_step" in bench:
+        sweep = ", ".join(f"{x['sequences']}: {x['us_per_step']:.2f}" for x in bench["batch_sweep"])
+        L.append(f"bench.py's own figures ({where}): "
+                 f"{bench['device_us_per_step']:.2f} us per step on the device (HIP events "
+                 f"around each graph replay), {bench['eager_us_per_step']:.1f} us per step when "
+                 f"the host launches every step; batch-size sweep (sequences: us per step) "
+                 f"{sweep}.  The tracer adds its own work between dispatches, so for steps "
+                 "this short the figures of a run without it are the ones to quote.\n")
     open(out_md, "w").write("\n".join(L) + "\n")
     print(f"wrote {out_md}")
 
@@ -1323,27 +1348,80 @@ def reduce_counters(fetch_csv, write_csv, plan_path, fetch_cmd, write_cmd, out_d
         print(f"wrote {out}")
 
 
+CACHE_COUNTERS = ("TCC_HIT_sum", "TCC_MISS_sum", "TCP_UTCL1_TRANSLATION_MISS_sum",
+                  "TCP_UTCL1_TRANSLATION_HIT_sum")
+
+
+def reduce_cache(pmc_csv, plan_path, out_md, profile_cmd):
+    """profiles/probe_cache_<workload>.md from one counter pass with the L2
+    hit/miss and first-level translation counters."""
+    import statistics as st
+    plan = json.load(open(plan_path))
+    rows = _read_csv(pmc_csv)
+    per = {c: _by_phase([r for r in rows if r["Counter_Name"] == c], plan)
+           for c in CACHE_COUNTERS}
+    n_tok = None
+    from workloads import CONFIGS
+    cfg = CONFIGS[plan["config"]]
+    n_tok = cfg.n_tok
+    labels = [("serial_timed", "k_lookup", "lookup (serial)"),
+              ("pipelined_timed", "k_pipelined", "pipelined step, Zipf ids"),
+              ("noreuse_timed", "k_pipelined", "pipelined step, uniform ids"),
+              ("serial_timed", "k_gather", "gather, Zipf ids (serial)"),
+              ("fused_timed", "k_embed", "fused lookup+gather"),
+              ("uniform_timed", "k_gather", "gather, uniform ids"),
+              ("contiguous_timed", "k_gather", "gather, contiguous rows")]
+    L = [f"# L2 hit rate and address-translation misses: {plan['config']} ({plan['workload']})\n",
+         "One counter pass (one MI355X; TCC_HIT/TCC_MISS are L2 requests summed over all "
+         "channels of the eight XCDs, TCP_UTCL1_TRANSLATION_* the first-level address "
+         "translation caches of the compute units):\n", f"    {profile_cmd}\n",
+         "Reduced with `python bench.py --reduce-cache <counter csv> --plan <plan.json> "
+         "--out <this file>`.\n",
+         f"Means per dispatch over each phase's {plan['steps']} timed launches "
+         f"({n_tok} tokens per launch):\n", "```"]
+    for phase, kern, label in labels:
+        vals = {}
+        for c in CACHE_COUNTERS:
+            v = [float(r["Counter_Value"]) for r in per[c].get(phase, [])
+                 if _short(r["Kernel_Name"]).startswith(kern)]
+            vals[c] = st.mean(v) if v else None
+        if any(v is None for v in vals.values()):
+            continue
+        h, mi = vals["TCC_HIT_sum"], vals["TCC_MISS_sum"]
+        tm = vals["TCP_UTCL1_TRANSLATION_MISS_sum"]
+        L.append(f"{label:30s} {kern:12s} L2 requests {h + mi:11.0f}  L2 hit "
+                 f"{h / max(h + mi, 1):6.1%}  UTCL1 misses {tm:9.0f} ({tm / n_tok:.3f} per token)")
+    L.append("```\n")
+    open(out_md, "w").write("\n".join(L) + "\n")
+    print(f"wrote {out_md}")
+
+
 def reduce_main(argv):
     ap = argparse.ArgumentParser(description="reduce rocprofv3 csv output of a bench.py run")
     ap.add_argument("--reduce-trace", metavar="KERNEL_TRACE_CSV")
     ap.add_argument("--reduce-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
+    ap.add_argument("--reduce-cache", metavar="COUNTER_CSV")
     ap.add_argument("--plan", required=True)
     ap.add_argument("--bench-json")
     ap.add_argument("--out")
     ap.add_argument("--profile-cmd", default="", help="the profiler command (trace)")
+    ap.add_argument("--bench-plain", action="store_true",
+                    help="--bench-json comes from a run without the profiler")
     ap.add_argument("--fetch-cmd", default="")
     ap.add_argument("--write-cmd", default="")
     ap.add_argument("--out-dir", default=os.path.join(ROOT, "profiles"))
     a = ap.parse_args(argv)
     if a.reduce_trace:
-        reduce_trace(a.reduce_trace, a.plan, a.bench_json, a.out, a.profile_cmd)
+        reduce_trace(a.reduce_trace, a.plan, a.bench_json, a.out, a.profile_cmd, a.bench_plain)
     if a.reduce_counters:
         reduce_counters(a.reduce_counters[0], a.reduce_counters[1], a.plan, a.fetch_cmd,
                         a.write_cmd, a.out_dir)
+    if a.reduce_cache:
+        reduce_cache(a.reduce_cache, a.plan, a.out, a.profile_cmd)
 
 
 def main():
-    if any(a in ("--reduce-trace", "--reduce-counters") for a in sys.argv[1:]):
+    if any(a in ("--reduce-trace", "--reduce-counters", "--reduce-cache") for a in sys.argv[1:]):
         reduce_main(sys.argv[1:])
         return
     ap = argparse.ArgumentParser()
