@@ -290,11 +290,34 @@ def probes_per_position(cfg, w, X: np.ndarray) -> float:
     return float(probes.sum()) / X.size
 
 
+def oracle_all_cores(one_pass, X: np.ndarray, min_seconds: float) -> dict:
+    """The oracle's passes over X with its rows split into one slice per host
+    thread (the oracle's calls release the interpreter lock, so the slices
+    run in parallel on its shared read-only dictionary), repeated for at least
+    min_seconds: a labelled all-core figure beside the single-core baseline."""
+    import threading
+    nthr = min(oracle_threads(), X.shape[0])
+    slices = np.array_split(np.arange(X.shape[0]), nthr)
+    passes, elapsed = 0, 0.0
+    while elapsed < min_seconds or passes == 0:
+        t = time.perf_counter()
+        th = [threading.Thread(target=one_pass, args=(X[sl],)) for sl in slices]
+        for x in th:
+            x.start()
+        for x in th:
+            x.join()
+        elapsed += time.perf_counter() - t
+        passes += 1
+    return {"value": passes * X.size / elapsed, "unit": "tokens/s", "threads": nthr,
+            "passes": passes, "seconds": round(elapsed, 3),
+            "how": f"the same passes with the rows split over {nthr} threads sharing the "
+                   "oracle's dictionary"}
+
+
 def cpu_baseline(cfg, w, X0, host_np_full, E, gpu_ids, gpu_outs, min_seconds: float):
     """Time the oracle (single-threaded) on batch 0, repeated until min_seconds,
     then the same passes split by rows over all host cores (labelled), and
     check the GPU results of batch 0 against it."""
-    import threading
     import torch
     import oracle
     from workloads import table_rows
@@ -328,21 +351,7 @@ def cpu_baseline(cfg, w, X0, host_np_full, E, gpu_ids, gpu_outs, min_seconds: fl
         out = one_pass(X0)
         elapsed += time.perf_counter() - t
         passes += 1
-    # All host cores: the rows of batch 0 split into one slice per thread
-    # (the oracle's calls release the interpreter lock, so slices run in
-    # parallel on a shared read-only dictionary).
-    nthr = min(oracle_threads(), X0.shape[0])
-    slices = np.array_split(np.arange(X0.shape[0]), nthr)
-    mt_passes, mt_elapsed = 0, 0.0
-    while mt_elapsed < min_seconds / 2 or mt_passes == 0:
-        t = time.perf_counter()
-        th = [threading.Thread(target=one_pass, args=(X0[sl],)) for sl in slices]
-        for x in th:
-            x.start()
-        for x in th:
-            x.join()
-        mt_elapsed += time.perf_counter() - t
-        mt_passes += 1
+    all_cores = oracle_all_cores(one_pass, X0, min_seconds / 2)
     parity_rows = [bool(g.view(torch.uint8).cpu().numpy().reshape(out.shape).tobytes()
                         == out.tobytes()) for g in gpu_outs]
     info = host_info()
@@ -353,11 +362,7 @@ def cpu_baseline(cfg, w, X0, host_np_full, E, gpu_ids, gpu_outs, min_seconds: fl
                        f"({build_s:.1f} s) not timed",
              "seconds": round(elapsed, 3), "build_seconds": round(build_s, 3),
              "cpu_model": info["cpu_model"], "cores_available": info["cores_available"],
-             "all_cores": {"value": mt_passes * cfg.n_tok / mt_elapsed, "unit": "tokens/s",
-                           "threads": nthr, "passes": mt_passes,
-                           "seconds": round(mt_elapsed, 3),
-                           "how": "the same passes with the rows of batch 0 split over "
-                                  f"{nthr} threads sharing the oracle's dictionary"}},
+             "all_cores": all_cores},
             {"ids_bit_exact": bool(np.array_equal(gpu_ids, exp_ids)),
              "split_rows_bit_exact": parity_rows[0], "fused_rows_bit_exact": parity_rows[1],
              "pipelined_rows_bit_exact": parity_rows[2],
@@ -884,13 +889,17 @@ def run_decode(args, cfg):
         uniq = np.unique(exp_ids)
         compact = table_rows(cfg, torch.from_numpy(uniq.astype(np.int64)),
                              device="cuda").cpu().view(torch.uint8).numpy()
+        def one_pass(rows):
+            ids_p, _ = o.lookup(rows, cfg.max_n)
+            oracle.gather(np.searchsorted(uniq, ids_p).astype(np.int32), compact)
+
         passes, elapsed = 0, 0.0
         while elapsed < args.cpu_seconds or passes == 0:
             t = time.perf_counter()
-            ids_p, _ = o.lookup(w.tokens, cfg.max_n)
-            oracle.gather(np.searchsorted(uniq, ids_p).astype(np.int32), compact)
+            one_pass(w.tokens)
             elapsed += time.perf_counter() - t
             passes += 1
+        all_cores = oracle_all_cores(one_pass, w.tokens, args.cpu_seconds / 2)
         # rows of the last step (left in `out` by the graph replay), byte for byte
         last = oracle.gather(np.searchsorted(uniq, exp_ids[:, -1]).astype(np.int32), compact)
         clen.fill_(0)
@@ -904,7 +913,7 @@ def run_decode(args, cfg):
                       f"(equal to decoding them), {passes} passes, memcpy gather from a compact "
                       f"host table of the {len(uniq)} referenced rows (id remap timed); "
                       f"dictionary build ({build_o:.1f} s) not timed",
-            "seconds": round(elapsed, 3)}
+            "seconds": round(elapsed, 3), **host_info(), "all_cores": all_cores}
         result["parity"] = {
             "ids_bit_exact": bool(np.array_equal(ids_eager.T, exp_ids)),
             "match_len_bit_exact": bool(np.array_equal(lens.cpu().numpy().T, exp_len)),
@@ -971,7 +980,8 @@ def run_tag(args, cfg):
         result["cpu_baseline"] = {"value": passes * sample.size / el, "unit": "tokens/s",
                                   "cores": 1, "kind": "oracle",
                                   "sample": f"the first {sample.shape[0]} sequences "
-                                            f"({sample.size} tokens), {passes} passes"}
+                                            f"({sample.size} tokens), {passes} passes",
+                                  **host_info()}
         result["parity"] = {"match_len_bit_exact": bool(np.array_equal(
             ml[:cfg.B].cpu().numpy(), exp_len))}
     return result
@@ -1018,7 +1028,8 @@ def run_discover(args, cfg):
         result["cpu_baseline"] = {"value": sample.size / el, "unit": "tokens/s", "cores": 1,
                                   "kind": "oracle",
                                   "sample": f"the first {sample.shape[0]} sequences "
-                                            f"({sample.size} tokens), counting with numpy"}
+                                            f"({sample.size} tokens), counting with numpy",
+                                  **host_info()}
         fg2, ln2, ct2 = S.discover_fgrams(torch.from_numpy(sample).to(dev), K, Sn, mc)
         got = {tuple(int(v) for v in r[:L]): int(c) for r, L, c in
                zip(fg2.cpu().numpy(), ln2.cpu().numpy(), ct2.cpu().numpy())}
@@ -1135,7 +1146,8 @@ def run_precompute(args, cfg):
         result["cpu_baseline"] = {"value": reps * len(cs) / el, "unit": "f-grams/s",
                                   "cores": blas_threads(), "kind": "oracle",
                                   "sample": f"{len(cs)} f-grams, repeated {reps} times, "
-                                            "float64 numpy (BLAS threads)"}
+                                            "float64 numpy (BLAS threads)",
+                                  "cpu_model": host_info()["cpu_model"]}
     return result
 
 
