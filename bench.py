@@ -1051,18 +1051,21 @@ def blas_threads() -> int:
         return 1
 
 
-def fgram_model_flops(lengths: np.ndarray, d: int, d_ff: int, n_layers: int) -> float:
+def fgram_model_flops(lengths: np.ndarray, d: int, d_ff: int, n_layers: int,
+                      products_only: bool = False) -> float:
     """Algorithmic flops of precomputing F for f-grams of these lengths.  A
     full layer costs, per token, 2 (3d^2 + d^2 + 2 d d_ff) for its four
     products and 4 (i + 1) d for position i's scores and weighted sum.  F
     needs only the last token's output, so the last layer computes q, k, v
     for every token but attention, the output projection and the MLP for the
-    last position alone."""
+    last position alone.  products_only leaves out the attention terms (the
+    flops of the matrix products alone)."""
     if n_layers == 0:
         return 0.0
     n = lengths.astype(np.float64)
-    full = n * 2.0 * (4.0 * d * d + 2.0 * d * d_ff) + 4.0 * d * n * (n + 1) / 2
-    last = n * 2.0 * 3.0 * d * d + 2.0 * (d * d + 2.0 * d * d_ff) + 4.0 * d * n
+    att = 0.0 if products_only else 1.0
+    full = n * 2.0 * (4.0 * d * d + 2.0 * d * d_ff) + att * 4.0 * d * n * (n + 1) / 2
+    last = n * 2.0 * 3.0 * d * d + 2.0 * (d * d + 2.0 * d * d_ff) + att * 4.0 * d * n
     return float((n_layers - 1) * full.sum() + last.sum())
 
 
@@ -1114,6 +1117,8 @@ def run_precompute(args, cfg):
                          "n_fgrams": n, "tokens": int(w.lengths.sum()), "d": mc.d,
                          "d_ff": mc.d_ff, "n_layers": mc.n_layers, "n_heads": mc.n_heads},
               "device_ms_per_step": dev_ms, "flops_per_step": flops, "TFLOPs": tflops,
+              "product_flops_per_step": fgram_model_flops(w.lengths, mc.d, mc.d_ff,
+                                                          mc.n_layers, products_only=True),
               "roofline": {"bound": "mfma", "achieved": tflops, "peak": MFMA_BF16_PEAK_TFLOPS,
                            "unit": "TFLOP/s", "frac": tflops / MFMA_BF16_PEAK_TFLOPS,
                            "traffic": None,
@@ -1360,6 +1365,81 @@ def reduce_counters(fetch_csv, write_csv, plan_path, fetch_cmd, write_cmd, out_d
         print(f"wrote {out}")
 
 
+def reduce_precompute(trace_csv, bench_json, pmc_csv, out_md, trace_cmd, pmc_cmd):
+    """profiles/fgram_model_<workload>_kernel_trace.md from a --kernel-trace run
+    of `bench.py --precompute` (one warm-up and two timed calls) and, when
+    given, a counter run with GRBM_GUI_ACTIVE, SQ_VALU_MFMA_BUSY_CYCLES,
+    SQ_INSTS_MFMA and SQ_BUSY_CYCLES."""
+    import collections
+    import statistics as st
+    bench = [json.loads(ln) for ln in open(bench_json) if ln.startswith('{"metric"')][0]
+    calls = bench["steps"] + bench["warmup"]
+    rows = [r for r in _read_csv(trace_csv) if "scone::" in r["Kernel_Name"]]
+    for r in rows:
+        r["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        r["short"] = _short(r["Kernel_Name"]).replace("gemm::", "")
+
+    def cls(name):
+        return {"k_gemm<0": "products: q/k/v (bias)", "k_gemm<1": "products: fc1 (bias+GELU)",
+                "k_gemm<2": "products: o-proj / fc2 (residual)"}.get(name[:8], name.split("<")[0])
+
+    by, tot = collections.defaultdict(list), collections.defaultdict(float)
+    for r in rows:
+        by[(r["short"], r["Grid_Size_X"])].append(r)
+        tot[cls(r["short"])] += r["ns"]
+    prod_ns = sum(v for k, v in tot.items() if k.startswith("products")) / calls
+    all_ns = sum(tot.values()) / calls
+    L = ["# Kernel trace: precompute of F (scone_fgram_model_forward)\n",
+         f"Workload: {bench['config']['workload']}; {bench['config']['n_fgrams']} f-grams, "
+         f"{bench['config']['tokens']} tokens; {bench['warmup']} warm-up and "
+         f"{bench['steps']} timed calls.\n",
+         "Commands (one MI355X, `<repo>` the repository root):\n", f"    {trace_cmd}"]
+    if pmc_csv:
+        L.append(f"    {pmc_cmd}")
+    L += ["", "Reduced with `python bench.py --reduce-precompute <trace csv> --bench-json "
+          "<bench stdout> [--pmc <counter csv>] --out <this file>`.\n",
+          "Sources (sha1): " + ", ".join(f"{x} {source_sha(x)}" for x in
+                                         ("fgram_model.hip", "gemm_bf16.h")) + ".\n",
+          "Per-kernel durations (ns), one line per (kernel, grid):\n", "```"]
+    for (name, grid), rs in sorted(by.items(), key=lambda kv: -sum(x["ns"] for x in kv[1])):
+        v = [x["ns"] for x in rs]
+        L.append(f"{name[:40]:40s} calls={len(rs):5d} avg_ns={st.mean(v):10.1f} "
+                 f"med_ns={st.median(v):10.1f} min_ns={min(v):9d} max_ns={max(v):9d} "
+                 f"grid={grid} wg={rs[0]['Workgroup_Size_X']} vgpr={rs[0]['VGPR_Count']} "
+                 f"lds={rs[0]['LDS_Block_Size']}")
+    L += ["```\n", f"Device time per call by kernel class (sum over the {calls} calls / "
+                   f"{calls}):\n", "```"]
+    for k, v in sorted(tot.items(), key=lambda kv: -kv[1]):
+        L.append(f"{k:36s} {v / calls / 1e6:8.2f} ms/call {100 * v / sum(tot.values()):6.1f}%")
+    L += [f"{'total':36s} {all_ns / 1e6:8.2f} ms/call", "```\n"]
+    pf = bench["product_flops_per_step"]
+    L.append(f"Matrix products: {pf / 1e12:.1f} TFLOP of algorithmic work per call in "
+             f"{prod_ns / 1e6:.1f} ms of k_gemm time, {pf / prod_ns / 1e3:.0f} TFLOP/s "
+             f"({100 * pf / prod_ns / 1e3 / 2500:.1f}% of the 2.5 PFLOP/s dense bf16 peak).  "
+             f"Whole call: {bench['flops_per_step'] / 1e12:.1f} TFLOP in {all_ns / 1e6:.1f} ms "
+             f"of kernel time, {bench['flops_per_step'] / all_ns / 1e3:.0f} TFLOP/s; bench.py's "
+             f"HIP events around each call read {bench['device_ms_per_step']:.1f} ms "
+             f"({bench['TFLOPs']:.0f} TFLOP/s).\n")
+    if pmc_csv:
+        pm = collections.defaultdict(dict)
+        for r in _read_csv(pmc_csv):
+            if "k_gemm" not in r["Kernel_Name"]:
+                continue
+            pm[int(r["Dispatch_Id"])][r["Counter_Name"]] = float(r["Counter_Value"])
+        # GRBM_GUI_ACTIVE counts each of the 8 XCDs' active cycles;
+        # SQ_VALU_MFMA_BUSY_CYCLES sums the matrix-core busy cycles of all
+        # 1,024 SIMDs (256 compute units x 4).
+        gui = sum(d.get("GRBM_GUI_ACTIVE", 0) for d in pm.values()) / 8
+        busy = sum(d.get("SQ_VALU_MFMA_BUSY_CYCLES", 0) for d in pm.values()) / 1024
+        mf = sum(d.get("SQ_INSTS_MFMA", 0) for d in pm.values())
+        L.append(f"Counter run over the products' {len(pm)} dispatches: the matrix cores are "
+                 f"busy {100 * busy / max(gui, 1):.1f}% of the active cycles "
+                 f"(SQ_VALU_MFMA_BUSY_CYCLES / 1,024 SIMDs over GRBM_GUI_ACTIVE / 8 XCDs); "
+                 f"{mf:.4g} MFMA instructions.\n")
+    open(out_md, "w").write("\n".join(L) + "\n")
+    print(f"wrote {out_md}")
+
+
 CACHE_COUNTERS = ("TCC_HIT_sum", "TCC_MISS_sum", "TCP_UTCL1_TRANSLATION_MISS_sum",
                   "TCP_UTCL1_TRANSLATION_HIT_sum")
 
@@ -1413,7 +1493,10 @@ def reduce_main(argv):
     ap.add_argument("--reduce-trace", metavar="KERNEL_TRACE_CSV")
     ap.add_argument("--reduce-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--reduce-cache", metavar="COUNTER_CSV")
-    ap.add_argument("--plan", required=True)
+    ap.add_argument("--reduce-precompute", metavar="KERNEL_TRACE_CSV")
+    ap.add_argument("--pmc", metavar="COUNTER_CSV")
+    ap.add_argument("--pmc-cmd", default="")
+    ap.add_argument("--plan")
     ap.add_argument("--bench-json")
     ap.add_argument("--out")
     ap.add_argument("--profile-cmd", default="", help="the profiler command (trace)")
@@ -1430,10 +1513,14 @@ def reduce_main(argv):
                         a.write_cmd, a.out_dir)
     if a.reduce_cache:
         reduce_cache(a.reduce_cache, a.plan, a.out, a.profile_cmd)
+    if a.reduce_precompute:
+        reduce_precompute(a.reduce_precompute, a.bench_json, a.pmc, a.out, a.profile_cmd,
+                          a.pmc_cmd)
 
 
 def main():
-    if any(a in ("--reduce-trace", "--reduce-counters", "--reduce-cache") for a in sys.argv[1:]):
+    if any(a in ("--reduce-trace", "--reduce-counters", "--reduce-cache", "--reduce-precompute")
+           for a in sys.argv[1:]):
         reduce_main(sys.argv[1:])
         return
     ap = argparse.ArgumentParser()

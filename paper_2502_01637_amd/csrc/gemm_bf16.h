@@ -21,6 +21,13 @@
 // four accumulators are four consecutive n of one row m: the epilogue writes
 // 8 bytes (bf16) or 16 bytes (f32) per lane per tile.
 //
+// Bias-only products (kBias) stage the finished bf16 tile in LDS after the
+// last slab and store it row by row: a lane's accumulators hold 4 consecutive
+// n of one row m, so written straight from registers a row gets 32 bytes per
+// store instruction; through LDS each store instruction writes whole 256-byte
+// row segments (measured 6-15% faster on the q/k/v product, no faster with the
+// GELU or residual epilogues, which keep the direct stores).
+//
 // LDS layout: a slab row is 64 elements = 128 bytes = eight 16-byte chunks,
 // stored at slot chunk ^ (row & 7).  A fragment read touches 16 consecutive
 // rows at one chunk; with this swizzle the LDS bank-conflict counter reads
@@ -89,7 +96,7 @@ constexpr int kWaitLds = 0xF | (7 << 4) | (0 << 8) | (3 << 14);
 constexpr int kBK = 64;        // k-slab depth (elements)
 constexpr int kRowBytes = 128;  // one slab row in LDS
 
-template <int EPI, int BM, int BN, int WGM, int WGN>
+template <int EPI, int BM, int BN, int WGM, int WGN, bool kStaged>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restrict__ A,
                                                          const uint16_t* __restrict__ W,
                                                          const uint16_t* __restrict__ bias,
@@ -101,7 +108,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
     constexpr int STAGE = (BM + BN) * kRowBytes;
     constexpr int GA = BM / 8 / NW, GW = BN / 8 / NW;  // 8-row copy groups per wavefront
     static_assert(GA * 8 * NW == BM && GW * 8 * NW == BN, "copy groups must split evenly");
-    __shared__ __attribute__((aligned(1024))) uint8_t smem[2 * STAGE];
+    static_assert(!kStaged || EPI == kBias, "only the bias epilogue is staged");
+    constexpr int ERS = WTN * 2 + 16;  // staged row stride: 16 bytes of padding per row
+    constexpr int SMEM = kStaged && NW * WTM * ERS > 2 * STAGE ? NW * WTM * ERS : 2 * STAGE;
+    __shared__ __attribute__((aligned(1024))) uint8_t smem[SMEM];
 
     // Consecutive workgroups land on different XCDs; renumber so that each
     // XCD walks a contiguous run of tiles (n fastest), which keeps the A rows
@@ -214,6 +224,39 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
 #pragma unroll
     for (int i = 0; i < TN; ++i)
         bb[i] = *reinterpret_cast<const u32x2*>(bias + n0 + wn * WTN + i * 16 + (lane >> 4) * 4);
+    if constexpr (kStaged) {
+        // Every wavefront is done reading slabs before any overwrites them.
+        __builtin_amdgcn_s_waitcnt(kWaitLds);
+        __builtin_amdgcn_s_barrier();
+        uint8_t* wb = smem + wave * (WTM * ERS);  // this wavefront's WTM x WTN part
+#pragma unroll
+        for (int i = 0; i < TN; ++i) {
+            const float b0 = bf16_to_f32(bb[i].x & 0xFFFFu), b1 = bf16_to_f32(bb[i].x >> 16);
+            const float b2 = bf16_to_f32(bb[i].y & 0xFFFFu), b3 = bf16_to_f32(bb[i].y >> 16);
+#pragma unroll
+            for (int j = 0; j < TM; ++j) {
+                u32x2 o;
+                o.x = pack_bf16x2(acc[i][j][0] + b0, acc[i][j][1] + b1);
+                o.y = pack_bf16x2(acc[i][j][2] + b2, acc[i][j][3] + b3);
+                *reinterpret_cast<u32x2*>(wb + (j * 16 + (lane & 15)) * ERS +
+                                          (i * 16 + (lane >> 4) * 4) * 2) = o;
+            }
+        }
+        __builtin_amdgcn_s_waitcnt(kWaitLds);
+        constexpr int LPR = WTN * 2 / 16;  // lanes per row, 16 bytes each
+        constexpr int RPI = 64 / LPR;      // rows per store instruction
+        const int rr = lane / LPR, cc = lane % LPR;
+        uint16_t* ob = static_cast<uint16_t*>(out);
+#pragma unroll
+        for (int it = 0; it < WTM / RPI; ++it) {
+            const int r = it * RPI + rr;
+            const int m = m0 + wm * WTM + r;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(wb + r * ERS + cc * 16);
+            if (m < M)
+                *reinterpret_cast<u32x4*>(ob + (int64_t)m * ldc + n0 + wn * WTN + cc * 8) = v;
+        }
+        return;
+    }
 #pragma unroll
     for (int i = 0; i < TN; ++i) {
         const int n = n0 + wn * WTN + i * 16 + (lane >> 4) * 4;
@@ -274,8 +317,14 @@ inline hipError_t launch_tiles(const uint16_t* A, const uint16_t* W, const uint1
                                void* out, int64_t ldc, int M, int N, int K, hipStream_t st) {
     const int tiles_n = N / BN;
     const int tiles_m = (M + BM - 1) / BM;
-    hipLaunchKernelGGL((k_gemm<EPI, BM, BN, WGM, WGN>), dim3((unsigned)(tiles_m * tiles_n)),
-                       dim3(64 * WGM * WGN), 0, st, A, W, bias, out, ldc, M, N, K, tiles_n);
+    const dim3 grid((unsigned)(tiles_m * tiles_n)), block(64 * WGM * WGN);
+    // The staged store writes 16-byte pieces: rows must start 16-byte aligned.
+    if (EPI == kBias && ldc % 8 == 0 && (uintptr_t)out % 16 == 0)
+        hipLaunchKernelGGL((k_gemm<EPI, BM, BN, WGM, WGN, EPI == kBias>), grid, block, 0, st, A,
+                           W, bias, out, ldc, M, N, K, tiles_n);
+    else
+        hipLaunchKernelGGL((k_gemm<EPI, BM, BN, WGM, WGN, false>), grid, block, 0, st, A, W,
+                           bias, out, ldc, M, N, K, tiles_n);
     return hipGetLastError();
 }
 

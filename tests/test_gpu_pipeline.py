@@ -171,3 +171,33 @@ def test_pipelined_errors_and_overlap():
     # nothing to do
     assert S.embed_pipelined(tb, None, 3, None, None, E) is None
     S.check_ok()
+
+
+@pytest.mark.parametrize("d", [1024, 2048, 4096])   # 2, 4 and 8 KiB rows (whole, 2- and 4-way split)
+def test_split_row_copies_zero_bad_rows(d):
+    """Rows of 4 and 8 KiB are copied in parts by several wavefronts: every
+    part of a row with a bad id is zeroed, the error is raised, and the other
+    rows are exact, in the standalone gather and in the pipelined step."""
+    rng = np.random.default_rng(d)
+    n_rows, n_tok = 97, 777
+    E = torch.from_numpy(rng.integers(-2**31, 2**31, size=(n_rows, d // 2), dtype=np.int64)
+                         .astype(np.int32)).cuda()
+    ids_np = rng.integers(0, n_rows, size=n_tok).astype(np.int32)
+    bad = rng.choice(n_tok, 40, replace=False)
+    ids_np[bad[:20]] = n_rows + rng.integers(0, 1000, 20)
+    ids_np[bad[20:]] = -1 - rng.integers(0, 1000, 20)
+    exp = E.cpu().numpy()[np.clip(ids_np, 0, n_rows - 1)]
+    exp[bad] = 0
+    ids = dev(ids_np)
+    out = S.gather(ids, E)
+    assert S.check() == S.scone.EROW
+    assert np.array_equal(out.cpu().numpy(), exp)
+    fg = np.array([[1, 2, -1]], dtype=np.int32)
+    tb = build_gpu(fg, [2], [5])
+    X = dev(np.arange(40, dtype=np.int32).reshape(2, 20) % 7)
+    nxt = torch.empty((2, 20), dtype=torch.int32, device="cuda")
+    outp = S.embed_pipelined(tb, X, 3, nxt, ids, E)
+    assert S.check() == S.scone.EROW
+    assert np.array_equal(outp.cpu().numpy(), exp)
+    exp_n = oracle.OracleTable(fg, [2], [5]).lookup(X.cpu().numpy(), 3)[0]
+    assert np.array_equal(nxt.cpu().numpy(), exp_n)
