@@ -1440,6 +1440,48 @@ def reduce_precompute(trace_csv, bench_json, pmc_csv, out_md, trace_cmd, pmc_cmd
     print(f"wrote {out_md}")
 
 
+def reduce_kernels(trace_csv, bench_json, plain_json, out_md, title, desc, cmd):
+    """A per-kernel summary of a --kernel-trace run of any bench.py mode (the
+    tagger and discovery summaries): this library's kernels by (name, grid),
+    their time per call, and bench.py's own figures from the profiled run and
+    from a run without the profiler."""
+    import collections
+    import statistics as st
+    rows = [r for r in _read_csv(trace_csv) if "scone::" in r["Kernel_Name"]]
+    by = collections.defaultdict(list)
+    for r in rows:
+        r["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        by[(_short(r["Kernel_Name"]), r["Grid_Size_X"])].append(r)
+    srcs = sorted(f for f in os.listdir(os.path.join(ROOT, "paper_2502_01637_amd", "csrc"))
+                  if f.endswith((".hip", ".h")))
+    L = [f"# Kernel trace: {title}\n", f"{desc}\n", "Command (one MI355X, `<repo>` the repository root):\n",
+         f"    {cmd}\n", "Reduced with `python bench.py --reduce-kernels <trace csv> --bench-json "
+         "<profiled run's stdout> --plain-json <stdout of a run without the profiler> ...`.\n",
+         "Sources (sha1): " + ", ".join(f"{x} {source_sha(x)}" for x in srcs) + ".\n",
+         "Per-kernel durations (ns), this library's kernels only:\n", "```"]
+    for (name, grid), rs in sorted(by.items(), key=lambda kv: -sum(x["ns"] for x in kv[1])):
+        v = [x["ns"] for x in rs]
+        L.append(f"{name[:48]:48s} calls={len(rs):5d} avg_ns={st.mean(v):11.1f} "
+                 f"med_ns={st.median(v):10.1f} min_ns={min(v):9d} max_ns={max(v):9d} "
+                 f"grid={grid} wg={rs[0]['Workgroup_Size_X']} vgpr={rs[0]['VGPR_Count']} "
+                 f"lds={rs[0]['LDS_Block_Size']}")
+    L.append("```\n")
+
+    def figures(path, where):
+        if not path:
+            return
+        b = [json.loads(ln) for ln in open(path) if ln.startswith('{"metric"')][0]
+        extra = "".join(f", {k} {b[k]:.4g}" for k in ("device_ms_per_pass", "ms_per_step")
+                        if k in b)
+        L.append(f"bench.py {where}: {b['value']:.4g} {b['unit']}{extra}.")
+
+    figures(bench_json, "under the profiler")
+    figures(plain_json, "without the profiler (a separate run in the same call)")
+    L.append("")
+    open(out_md, "w").write("\n".join(L) + "\n")
+    print(f"wrote {out_md}")
+
+
 CACHE_COUNTERS = ("TCC_HIT_sum", "TCC_MISS_sum", "TCP_UTCL1_TRANSLATION_MISS_sum",
                   "TCP_UTCL1_TRANSLATION_HIT_sum")
 
@@ -1494,6 +1536,10 @@ def reduce_main(argv):
     ap.add_argument("--reduce-counters", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"))
     ap.add_argument("--reduce-cache", metavar="COUNTER_CSV")
     ap.add_argument("--reduce-precompute", metavar="KERNEL_TRACE_CSV")
+    ap.add_argument("--reduce-kernels", metavar="KERNEL_TRACE_CSV")
+    ap.add_argument("--plain-json")
+    ap.add_argument("--title", default="")
+    ap.add_argument("--desc", default="")
     ap.add_argument("--pmc", metavar="COUNTER_CSV")
     ap.add_argument("--pmc-cmd", default="")
     ap.add_argument("--plan")
@@ -1513,14 +1559,17 @@ def reduce_main(argv):
                         a.write_cmd, a.out_dir)
     if a.reduce_cache:
         reduce_cache(a.reduce_cache, a.plan, a.out, a.profile_cmd)
+    if a.reduce_kernels:
+        reduce_kernels(a.reduce_kernels, a.bench_json, a.plain_json, a.out, a.title, a.desc,
+                       a.profile_cmd)
     if a.reduce_precompute:
         reduce_precompute(a.reduce_precompute, a.bench_json, a.pmc, a.out, a.profile_cmd,
                           a.pmc_cmd)
 
 
 def main():
-    if any(a in ("--reduce-trace", "--reduce-counters", "--reduce-cache", "--reduce-precompute")
-           for a in sys.argv[1:]):
+    if any(a in ("--reduce-trace", "--reduce-counters", "--reduce-cache", "--reduce-precompute",
+                 "--reduce-kernels") for a in sys.argv[1:]):
         reduce_main(sys.argv[1:])
         return
     ap = argparse.ArgumentParser()
