@@ -84,3 +84,42 @@ def test_static_split_beyond_scratch_launches_nothing(tables):
     assert static_split(ids, near, far, out, nu) == S.scone.ESCRATCH
     torch.cuda.synchronize()
     assert bool((out == 3.0).all()) and int(nu.item()) == -1
+
+
+def test_static_split_in_a_captured_graph(tables):
+    """The allocation-free call captured in a HIP graph (its use case: it
+    allocates nothing and launches kernels only) and replayed three times,
+    with other work on the same scratch between the replays; every replay
+    equals the eager result."""
+    near, far, concat = tables
+    rng = np.random.default_rng(9)
+    n_tok = 2048
+    ids_np = batch(rng, n_tok, 0, N_FAR)
+    ids = torch.from_numpy(ids_np).cuda()
+    other = torch.from_numpy(batch(rng, 3000, 0, N_FAR)).cuda()
+    eager = torch.empty((n_tok, D), dtype=torch.bfloat16, device="cuda")
+    nu = torch.zeros(1, dtype=torch.int32, device="cuda")
+    assert static_split(ids, near, far, eager, nu) == S.scone.OK
+    S.check_ok()
+    exp = oracle.gather(ids_np, concat)
+    assert eager.cpu().view(torch.uint8).numpy().tobytes() == exp.tobytes()
+    out = torch.zeros_like(eager)
+    nu_g = torch.zeros(1, dtype=torch.int32, device="cuda")
+    scratch_out = torch.empty((3000, D), dtype=torch.bfloat16, device="cuda")
+    nu_o = torch.zeros(1, dtype=torch.int32, device="cuda")
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            assert static_split(ids, near, far, out, nu_g) == S.scone.OK
+    torch.cuda.current_stream().wait_stream(s)
+    for r in range(3):
+        out.zero_()
+        # eager work that reuses the same scratch between replays
+        assert static_split(other, near, far, scratch_out, nu_o) == S.scone.OK
+        g.replay()
+        torch.cuda.synchronize()
+        S.check_ok()
+        assert torch.equal(out.view(torch.int16), eager.view(torch.int16)), r
+        assert int(nu_g.item()) == int(nu.item()), r
