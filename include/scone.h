@@ -117,8 +117,10 @@ int scone_build_fgram_table(const int32_t* fgrams, const int32_t* lengths,
  *  fgram_ids  [B, T] int32 output.
  *  match_len  [B, T] int8 output, or NULL.
  *
- * Asynchronous on `stream`; the table is read-only, so concurrent lookups on
- * one table are safe.  B * T = 0 launches nothing.
+ * Outputs that share memory with token_ids (or with each other) give
+ * SCONE_EINVAL: workgroups read a halo of tokens that other workgroups'
+ * positions own.  Asynchronous on `stream`; the table is read-only, so
+ * concurrent lookups on one table are safe.  B * T = 0 launches nothing.
  */
 int scone_lookup(const scone_table_t* table, const int32_t* token_ids, int64_t B,
                  int64_t T, int32_t max_n, int32_t* fgram_ids, int8_t* match_len,
@@ -137,7 +139,8 @@ int scone_lookup(const scone_table_t* table, const int32_t* token_ids, int64_t B
  *             hist[n] is INCREASED by the number of positions whose match
  *             length is n (the caller zeroes it to start a count).
  *
- * At least one of match_len and hist must be given.  Asynchronous.
+ * At least one of match_len and hist must be given; neither may share memory
+ * with token_ids or with the other (else SCONE_EINVAL).  Asynchronous.
  */
 int scone_tag(const scone_table_t* table, const int32_t* token_ids, int64_t B, int64_t T,
               int32_t max_n, int8_t* match_len, uint64_t* hist, void* stream);
@@ -154,7 +157,8 @@ int scone_tag(const scone_table_t* table, const int32_t* token_ids, int64_t B, i
  *             (SCONE_PLACE_HOST).
  *  row_bytes  > 0.  Rows move in 16-byte vectors when row_bytes and both
  *             pointers allow it, otherwise in the widest unit that does.
- *  out        [n_tok, row_bytes] device output; must not overlap `rows`.
+ *  out        [n_tok, row_bytes] device output; sharing memory with `rows`
+ *             or with fgram_ids gives SCONE_EINVAL.
  *
  * Asynchronous on `stream`.  n_tok = 0 launches nothing.
  */
@@ -173,7 +177,9 @@ int scone_gather(const int32_t* fgram_ids, int64_t n_tok, const void* rows,
  *  fgram_ids  [B, T] int32 output, or NULL when not wanted.
  *  match_len  [B, T] int8 output, or NULL.
  *
- * Errors as for scone_lookup and scone_gather.  Asynchronous on `stream`.
+ * Errors as for scone_lookup and scone_gather; out, fgram_ids and match_len
+ * may not share memory with token_ids, rows or each other (SCONE_EINVAL).
+ * Asynchronous on `stream`.
  */
 int scone_embed(const scone_table_t* table, const int32_t* token_ids, int64_t B, int64_t T,
                 int32_t max_n, const void* rows, int64_t n_rows, int64_t row_bytes,
@@ -200,9 +206,10 @@ int scone_embed(const scone_table_t* table, const int32_t* token_ids, int64_t B,
  *  rows, n_rows, row_bytes, placement   as for scone_gather.
  *  out        [n_cur, row_bytes] device output.
  *
- * Returns SCONE_EINVAL when next_ids or next_len share memory with cur_ids
- * (the launch writes one while it reads the other); otherwise errors as for
- * scone_lookup and scone_gather.  Rows of 1, 2, 4 or 8 KiB, 16-byte aligned,
+ * Returns SCONE_EINVAL when any output (next_ids, next_len, out) shares
+ * memory with an input (next_tokens, cur_ids) or with another output: the
+ * launch writes them while its other workgroups read; otherwise errors as
+ * for scone_lookup and scone_gather.  Rows of 1, 2, 4 or 8 KiB, 16-byte aligned,
  * take the one-launch kernel; other widths run the lookup and gather kernels
  * back to back with the same results.  Asynchronous on `stream`.
  */
@@ -230,8 +237,10 @@ int scone_embed_pipelined(const scone_table_t* table, const int32_t* next_tokens
  *  rows ...   as for scone_gather; out is [S, row_bytes].
  *  fgram_ids  [S] int32 output, or NULL; match_len [S] int8 or NULL.
  *
- * Asynchronous on `stream`.  Calls for the same sequences must be ordered
- * (the context is read and rewritten in place).
+ * out, fgram_ids and match_len may not share memory with ctx, ctx_len,
+ * new_tok, rows or each other, nor ctx, ctx_len and new_tok with each other
+ * (SCONE_EINVAL).  Asynchronous on `stream`.  Calls for the same sequences
+ * must be ordered (the context is read and rewritten in place).
  */
 int scone_decode_step(const scone_table_t* table, int32_t* ctx, int32_t* ctx_len,
                       int32_t ctx_cap, const int32_t* new_tok, int64_t S, int32_t max_n,
@@ -255,7 +264,8 @@ int scone_decode_step(const scone_table_t* table, int32_t* ctx, int32_t* ctx_len
  *              host-mapped (scone_host_alloc).  n_near + n_far <= 2^31.
  *  row_bytes   a multiple of 16; every pointer 16-byte aligned (else
  *              SCONE_EINVAL).
- *  out         [n_tok, row_bytes] device output.
+ *  out         [n_tok, row_bytes] device output; sharing memory with
+ *              fgram_ids or near_rows gives SCONE_EINVAL.
  *  workspace   device scratch of at least scone_gather_split_workspace(n_tok,
  *              row_bytes) bytes (else SCONE_EINVAL), caller-owned, reusable
  *              across calls that do not overlap.
