@@ -435,7 +435,9 @@ void scone_table_destroy(scone_table_t* table);
 /* Properties of a built table; any output pointer may be NULL.  n: f-grams
  * stored; capacity: slots; max_len: K; slot_bytes: 16 or 32; entries: slots
  * in use, the f-grams plus the flagged suffix markers (so entries / capacity
- * is the table's load). */
+ * is the table's load).  Two concurrent inserts of the same marker can leave
+ * two copies of it, so entries may differ slightly between builds of the same
+ * set; lookups are unaffected. */
 int scone_table_info(const scone_table_t* table, int64_t* n, int64_t* capacity,
                      int32_t* max_len, int32_t* slot_bytes, int64_t* entries);
 
