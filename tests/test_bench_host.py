@@ -103,10 +103,10 @@ def test_trace_reducer_takes_each_phase_from_its_own_dispatches(tmp_path):
     out = tmp_path / "trace.md"
     bench.reduce_trace(str(trace), str(plan), None, str(out), "rocprofv3 ... -- python bench.py")
     text = out.read_text()
-    assert "pipelined_timed   k_pipelined<16, 2, 4>" in text and "mean     1.00 us" in text
-    assert "noreuse_timed" in text and "mean     3.00 us" in text
-    assert "uniform_timed" in text and "mean     5.00 us" in text
-    assert "serial_timed      k_gather_rows<4>" in text and "mean     0.20 us" in text
+    assert "pipelined_timed   k_pipelined<16, 2, 4>" in text and "mean      1.00 us" in text
+    assert "noreuse_timed" in text and "mean      3.00 us" in text
+    assert "uniform_timed" in text and "mean      5.00 us" in text
+    assert "serial_timed      k_gather_rows<4>" in text and "mean      0.20 us" in text
     # a csv that disagrees with the plan is refused
     rows[3]["Kernel_Name"] = KNAMES["k_gather"]
     _write_csv(trace, list(rows[0].keys()), rows)
