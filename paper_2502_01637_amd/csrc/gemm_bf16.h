@@ -36,6 +36,8 @@
 // (8 whole rows), each lane fetching the chunk its slot must hold.
 #pragma once
 
+#include <type_traits>
+
 #include "scone_internal.h"
 
 namespace scone {
@@ -84,6 +86,16 @@ __device__ __forceinline__ float gelu_erf(float x) {
     const float e = __builtin_amdgcn_exp2f(-(z * z) * 1.4426950408889634f);  // exp(-z^2)
     const float erf_abs = 1.0f - q * t * e;
     return 0.5f * x * (1.0f + (x < 0.0f ? -erf_abs : erf_abs));
+}
+
+// The lane id, computed from the execution mask with an operand the
+// compiler cannot see through, so it is not merged with an earlier copy:
+// values derived from it are recomputed where they are used instead of being
+// held in registers (at 256 registers per lane, held values spill).
+__device__ __forceinline__ int fresh_lane() {
+    unsigned z = 0;
+    asm volatile("" : "+s"(z));
+    return (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, z));
 }
 
 // s_waitcnt immediates (gfx9 encoding): wait until at most n vector-memory
@@ -186,19 +198,43 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
                                                                     0, 0, 0);
     };
 
+    // Scheduling masks of __builtin_amdgcn_sched_group_barrier.
+    constexpr int kMfma = 0x008, kVmemRead = 0x020, kDsRead = 0x100;
+    constexpr int NR = TN + TM;  // fragment reads per half slab
+    constexpr int NP = TN * TM;  // products per half slab
+    static_assert(NP >= NR + GA + GW, "the interleave needs a product per read and copy");
     const int KT = K / kBK;
     bf16x8 f0w[TN], f0a[TM], f1w[TN], f1a[TM];  // halves 0 and 1 of a slab
+    u32x2 bb[TN];                                // this lane's biases, loaded in the last slab
     issue(0, 0);
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
     if (KT > 1) issue(1, 1);
     read(0, 0, f0w, f0a);
-    for (int kt = 0; kt < KT; ++kt) {
+    // One slab.  Half 0's products run with half 1's fragment reads slotted
+    // one after each product, so the reads overlap the products.  Issued as
+    // a block before the products, as the compiler orders them by itself, the
+    // reads were followed by a wait for every outstanding LDS read (the count
+    // covers all of them, the new ones included) and both wavefronts of a
+    // SIMD idled for an LDS round trip per slab.  When a next slab exists:
+    // the counted waits and the barrier, then half 1's products with the
+    // copies of slab kt + 2 and the next slab's half-0 reads slotted in the
+    // same way.  kNext / kIssue are compile-time so that each half is one
+    // straight run of code the scheduler can interleave.
+    auto step = [&](int kt, auto next_c, auto issue_c) {
+        constexpr bool kNext = decltype(next_c)::value;
+        constexpr bool kIssue = decltype(issue_c)::value;
         read(kt & 1, 1, f1w, f1a);
         multiply(f0w, f0a);
+#pragma unroll
+        for (int i = 0; i < NR; ++i) {
+            __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(kMfma, NP - NR, 0);
         __builtin_amdgcn_sched_barrier(0);
-        if (kt + 1 < KT) {
+        if constexpr (kNext) {
             // Half 1 of slab kt has landed, so this wavefront reads nothing
             // more from stage kt & 1, and its copies of slab kt + 1 are in
             // LDS; after the barrier the same holds for every wavefront:
@@ -207,23 +243,48 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
             __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
             __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_sched_barrier(0);
-            if (kt + 2 < KT) issue(kt + 2, kt & 1);
+            if constexpr (kIssue) issue(kt + 2, kt & 1);
             read((kt + 1) & 1, 0, f0w, f0a);
+        } else {
+            // Last slab: the epilogue's bias loads fly during half 1's
+            // products, in the registers half 0's fragments held.
+#pragma unroll
+            for (int i = 0; i < TN; ++i)
+                bb[i] = *reinterpret_cast<const u32x2*>(bias + n0 + wn * WTN + i * 16 +
+                                                         (lane >> 4) * 4);
         }
         multiply(f1w, f1a);
+        if constexpr (kNext) {
+            if constexpr (kIssue) {
+#pragma unroll
+                for (int i = 0; i < GA + GW; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(kMfma, 1, 1);
+                    __builtin_amdgcn_sched_group_barrier(kVmemRead, 1, 1);
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < NR; ++i) {
+                __builtin_amdgcn_sched_group_barrier(kMfma, 1, 1);
+                __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 1);
+            }
+            __builtin_amdgcn_sched_group_barrier(kMfma, NP - NR - (kIssue ? GA + GW : 0), 1);
+        }
         __builtin_amdgcn_sched_barrier(0);
-    }
+    };
+    int kt = 0;
+    for (; kt + 2 < KT; ++kt) step(kt, std::true_type{}, std::true_type{});
+    if (kt + 1 < KT) step(kt++, std::true_type{}, std::false_type{});
+    step(kt, std::false_type{}, std::false_type{});
 
+    // The epilogue takes a fresh lane id (see fresh_lane) so that no
+    // lane-derived value stays live through the main loop.
+    const int elane = fresh_lane();
     // acc[i][j][r] = C[m, n] with n = n0 + wn*WTN + i*16 + (lane/16)*4 + r and
     // m = m0 + wm*WTM + j*16 + lane%16.  Every load the epilogue needs (the
     // biases, and for kResid the residual values of up to four column groups)
     // is issued before its first use, so a wavefront waits once per round
     // instead of once per 16 x 16 tile; rows past M read row M - 1 and are
     // not stored.
-    u32x2 bb[TN];
-#pragma unroll
-    for (int i = 0; i < TN; ++i)
-        bb[i] = *reinterpret_cast<const u32x2*>(bias + n0 + wn * WTN + i * 16 + (lane >> 4) * 4);
     if constexpr (kStaged) {
         // Every wavefront is done reading slabs before any overwrites them.
         __builtin_amdgcn_s_waitcnt(kWaitLds);
@@ -238,14 +299,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
                 u32x2 o;
                 o.x = pack_bf16x2(acc[i][j][0] + b0, acc[i][j][1] + b1);
                 o.y = pack_bf16x2(acc[i][j][2] + b2, acc[i][j][3] + b3);
-                *reinterpret_cast<u32x2*>(wb + (j * 16 + (lane & 15)) * ERS +
-                                          (i * 16 + (lane >> 4) * 4) * 2) = o;
+                *reinterpret_cast<u32x2*>(wb + (j * 16 + (elane & 15)) * ERS +
+                                          (i * 16 + (elane >> 4) * 4) * 2) = o;
             }
         }
         __builtin_amdgcn_s_waitcnt(kWaitLds);
         constexpr int LPR = WTN * 2 / 16;  // lanes per row, 16 bytes each
         constexpr int RPI = 64 / LPR;      // rows per store instruction
-        const int rr = lane / LPR, cc = lane % LPR;
+        const int rr = elane / LPR, cc = elane % LPR;
         uint16_t* ob = static_cast<uint16_t*>(out);
 #pragma unroll
         for (int it = 0; it < WTM / RPI; ++it) {
@@ -259,7 +320,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
     }
 #pragma unroll
     for (int i = 0; i < TN; ++i) {
-        const int n = n0 + wn * WTN + i * 16 + (lane >> 4) * 4;
+        const int n = n0 + wn * WTN + i * 16 + (elane >> 4) * 4;
         const float b0 = bf16_to_f32(bb[i].x & 0xFFFFu), b1 = bf16_to_f32(bb[i].x >> 16);
         const float b2 = bf16_to_f32(bb[i].y & 0xFFFFu), b3 = bf16_to_f32(bb[i].y >> 16);
         if (EPI == kResid) {
@@ -273,7 +334,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
             for (int g = 0; g < G; ++g)
 #pragma unroll
                 for (int j = 0; j < TM; ++j) {
-                    const int m = m0 + wm * WTM + j * 16 + (lane & 15);
+                    const int m = m0 + wm * WTM + j * 16 + (elane & 15);
                     h[g][j] = *reinterpret_cast<const f32x4*>(
                         o + (int64_t)(m < M ? m : M - 1) * ldc + n + g * 16);
                 }
@@ -284,7 +345,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
                 const float c2 = bf16_to_f32(bg.y & 0xFFFFu), c3 = bf16_to_f32(bg.y >> 16);
 #pragma unroll
                 for (int j = 0; j < TM; ++j) {
-                    const int m = m0 + wm * WTM + j * 16 + (lane & 15);
+                    const int m = m0 + wm * WTM + j * 16 + (elane & 15);
                     if (m >= M) continue;
                     h[g][j][0] += acc[i + g][j][0] + c0;
                     h[g][j][1] += acc[i + g][j][1] + c1;
@@ -296,7 +357,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
         } else {
 #pragma unroll
             for (int j = 0; j < TM; ++j) {
-                const int m = m0 + wm * WTM + j * 16 + (lane & 15);
+                const int m = m0 + wm * WTM + j * 16 + (elane & 15);
                 if (m >= M) continue;
                 float v0 = acc[i][j][0] + b0, v1 = acc[i][j][1] + b1;
                 float v2 = acc[i][j][2] + b2, v3 = acc[i][j][3] + b3;
