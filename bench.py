@@ -1440,6 +1440,28 @@ def reduce_precompute(trace_csv, bench_json, pmc_csv, out_md, trace_cmd, pmc_cmd
     print(f"wrote {out_md}")
 
 
+def kernel_sources(names):
+    """The library sources a set of kernels is built from: each file that
+    defines one of them (``name<...>`` or ``name``), the local headers those
+    files include, and the runtime (the error word)."""
+    import re
+    csrc = os.path.join(ROOT, "paper_2502_01637_amd", "csrc")
+    files = sorted(f for f in os.listdir(csrc) if f.endswith((".hip", ".h")))
+    text = {f: open(os.path.join(csrc, f)).read() for f in files}
+    base = {n.split("<")[0] for n in names}
+    out = {"runtime.hip"}
+    for f in files:
+        if any(re.search(r"\bvoid\s+" + re.escape(b) + r"\s*\(", text[f]) for b in base):
+            out.add(f)
+    todo = list(out)
+    while todo:
+        for h in re.findall(r'#include "([\w.]+)"', text[todo.pop()]):
+            if h in text and h not in out:
+                out.add(h)
+                todo.append(h)
+    return sorted(out)
+
+
 def reduce_kernels(trace_csv, bench_json, plain_json, out_md, title, desc, cmd):
     """A per-kernel summary of a --kernel-trace run of any bench.py mode (the
     tagger and discovery summaries): this library's kernels by (name, grid),
@@ -1452,8 +1474,7 @@ def reduce_kernels(trace_csv, bench_json, plain_json, out_md, title, desc, cmd):
     for r in rows:
         r["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
         by[(_short(r["Kernel_Name"]), r["Grid_Size_X"])].append(r)
-    srcs = sorted(f for f in os.listdir(os.path.join(ROOT, "paper_2502_01637_amd", "csrc"))
-                  if f.endswith((".hip", ".h")))
+    srcs = kernel_sources({name for name, _ in by})
     L = [f"# Kernel trace: {title}\n", f"{desc}\n", "Command (one MI355X, `<repo>` the repository root):\n",
          f"    {cmd}\n", "Reduced with `python bench.py --reduce-kernels <trace csv> --bench-json "
          "<profiled run's stdout> --plain-json <stdout of a run without the profiler> ...`.\n",

@@ -155,3 +155,11 @@ def test_counter_reducer_calibrates_and_averages_timed_dispatches(tmp_path):
     assert rec["gather"]["uniform_traffic_bytes_per_launch"] == (700 * 2 + 700) * 1024
     assert rec["pipelined"]["source_sha1"] == bench.source_sha(*bench.KERNEL_SOURCES["pipelined"])
     assert cfg.n_tok > 0
+
+
+def test_kernel_sources_names_the_defining_files_and_their_headers():
+    srcs = bench.kernel_sources({"k_lookup<16, 2>", "k_mark<16>"})
+    assert {"lookup.hip", "tile_lookup.h", "table_build.hip", "scone_internal.h",
+            "runtime.hip"} <= set(srcs)
+    assert "gemm_bf16.h" not in srcs and "discover.hip" not in srcs
+    assert "gemm_bf16.h" in bench.kernel_sources({"k_gemm<1, 256, 256, 4, 2, false>"})
