@@ -268,9 +268,13 @@ int scone_decode_step(const scone_table_t* table, int32_t* ctx, int32_t* ctx_len
  *              fgram_ids or near_rows gives SCONE_EINVAL.
  *  workspace   device scratch of at least scone_gather_split_workspace(n_tok,
  *              row_bytes) bytes (else SCONE_EINVAL), caller-owned, reusable
- *              across calls that do not overlap.
+ *              across calls that do not overlap.  The part of it the call
+ *              uses (scone_gather_split_workspace bytes) may not share memory
+ *              with fgram_ids, near_rows, far_rows, out or n_unique
+ *              (SCONE_EINVAL).
  *  n_unique    device int32 receiving the number of distinct far ids (the
- *              rows that crossed PCIe), or NULL.
+ *              rows that crossed PCIe), or NULL; sharing memory with out or
+ *              fgram_ids gives SCONE_EINVAL.
  *
  * Asynchronous on `stream`; launches kernels only (no memset or copy nodes),
  * so the call can be captured in a graph.

@@ -219,7 +219,8 @@ int split_run(const int32_t* fgram_ids, int64_t n_tok, const void* near_rows, in
 // Argument checks shared by both entry points (the workspace is checked by
 // each); SCONE_OK means the call has work to do.
 int split_args(const int32_t* fgram_ids, int64_t n_tok, const void* near_rows, int64_t n_near,
-               const void* far_rows, int64_t n_far, int64_t row_bytes, const void* out) {
+               const void* far_rows, int64_t n_far, int64_t row_bytes, const void* out,
+               const int32_t* n_unique) {
     if (n_tok < 0 || n_near < 0 || n_far < 0 || row_bytes <= 0) return SCONE_EINVAL;
     if (row_bytes % 16 != 0 ||
         ((uintptr_t)near_rows | (uintptr_t)far_rows | (uintptr_t)out) % 16 != 0)
@@ -231,6 +232,11 @@ int split_args(const int32_t* fgram_ids, int64_t n_tok, const void* near_rows, i
         return SCONE_EINVAL;
     if (overlaps(out, n_tok * row_bytes, fgram_ids, span_bytes(n_tok, 4)) ||
         overlaps(out, n_tok * row_bytes, near_rows, span_bytes(n_near, row_bytes)))
+        return SCONE_EINVAL;
+    // n_unique is written by the fetch kernel while the gather kernel still
+    // reads the ids and writes out.
+    if (overlaps(n_unique, 4, out, n_tok * row_bytes) ||
+        overlaps(n_unique, 4, fgram_ids, span_bytes(n_tok, 4)))
         return SCONE_EINVAL;
     return SCONE_OK;
 }
@@ -244,11 +250,20 @@ extern "C" int scone_gather_split(const int32_t* fgram_ids, int64_t n_tok, const
                                   int64_t workspace_bytes, int32_t* n_unique, void* stream) {
     using namespace scone;
     const int rc = split_args(fgram_ids, n_tok, near_rows, n_near, far_rows, n_far, row_bytes,
-                              out);
+                              out, n_unique);
     if (rc != SCONE_OK) return rc;
     if ((uintptr_t)workspace % 16 != 0) return SCONE_EINVAL;
     if (n_tok == 0) return SCONE_OK;
     if (!workspace) return SCONE_EINVAL;
+    // The kernels write the workspace while they read every input and write
+    // out and n_unique: it may share memory with none of them.
+    const int64_t used = layout(n_tok, row_bytes).total;
+    if (overlaps(workspace, used, fgram_ids, span_bytes(n_tok, 4)) ||
+        overlaps(workspace, used, near_rows, span_bytes(n_near, row_bytes)) ||
+        overlaps(workspace, used, far_rows, span_bytes(n_far, row_bytes)) ||
+        overlaps(workspace, used, out, n_tok * row_bytes) ||
+        overlaps(workspace, used, n_unique, 4))
+        return SCONE_EINVAL;
     return split_run(fgram_ids, n_tok, near_rows, n_near, far_rows, n_far, row_bytes, out,
                      workspace, workspace_bytes, n_unique, stream);
 }
@@ -291,7 +306,7 @@ extern "C" int scone_gather_split_static(const int32_t* fgram_ids, int64_t n_tok
                                          void* out, int32_t* n_unique, void* stream) {
     using namespace scone;
     const int rc = split_args(fgram_ids, n_tok, near_rows, n_near, far_rows, n_far, row_bytes,
-                              out);
+                              out, n_unique);
     if (rc != SCONE_OK) return rc;
     if (n_tok == 0) return SCONE_OK;
     if (layout(n_tok, row_bytes).total > (int64_t)SCONE_SPLIT_STATIC_BYTES) return SCONE_ESCRATCH;

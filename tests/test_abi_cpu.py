@@ -219,3 +219,32 @@ def test_static_split_gather_checks_its_scratch_limit_on_the_host():
     assert F(ids, 5, near, 10, far, 10, 24, out, None, None) == S.scone.EINVAL   # width % 16
     assert F(None, 5, near, 10, far, 10, R, out, None, None) == S.scone.EINVAL
     assert F(ids, 5, near, 10, far, 10, R, _fake((1 << 32) + 8), None, None) == S.scone.EINVAL
+
+
+def test_split_gather_rejects_workspace_and_count_aliasing():
+    """scone_gather_split's workspace (the part the call uses) may not share
+    memory with any input or output, and n_unique may not share memory with
+    out or the ids; the static variant checks n_unique the same way.  A call
+    whose buffers do not alias gets past the checks and only then fails here,
+    at its first HIP call."""
+    L = S.scone.lib()
+    E, H = S.scone.EINVAL, S.scone.EHIP
+    G, F = L.scone_gather_split, L.scone_gather_split_static
+    n, R, nn, nf = 100, 4096, 10, 10
+    ids, near, far, out = _fake(1 << 32), _fake(2 << 32), _fake(3 << 32), _fake(4 << 32)
+    cnt, ws = _fake(5 << 32), _fake(6 << 32)
+    need = L.scone_gather_split_workspace(n, R)
+    assert need > n * R
+    assert G(ids, n, near, nn, far, nf, R, out, ws, need, cnt, None) == H
+    assert G(ids, n, near, nn, far, nf, R, out, ws, need - 16, cnt, None) == E  # too small
+    for bad in ((1 << 32) - need + 16,            # workspace ends inside the ids
+                (2 << 32) + 16 * (nn * R // 16 - 1),   # starts inside near_rows
+                (3 << 32) - 16,                   # runs into far_rows
+                (4 << 32) + 1024 * 16,            # starts inside out
+                (5 << 32) - need + 16):           # ends inside n_unique
+        assert G(ids, n, near, nn, far, nf, R, out, _fake(bad), need, cnt, None) == E, bad
+    # n_unique inside out or inside the ids, for both entry points
+    for c in (_fake((4 << 32) + 4096), _fake((1 << 32) + 8)):
+        assert G(ids, n, near, nn, far, nf, R, out, ws, need, c, None) == E
+        assert F(ids, n, near, nn, far, nf, R, out, c, None) == E
+    assert F(ids, n, near, nn, far, nf, R, out, cnt, None) == H
