@@ -334,6 +334,8 @@ int scone_gather_split_static(const int32_t* fgram_ids, int64_t n_tok, const voi
  *             across calls that do not overlap (else SCONE_EINVAL); or NULL,
  *             and the call allocates that much itself and frees it before
  *             returning.
+ * No two of token_ids, fgrams, lengths, counts and the workspace (the part
+ * the call uses) may share memory (SCONE_EINVAL).
  *
  * The output is ready for scone_build_fgram_table (ids are the caller's
  * choice).  Synchronous (it reads the candidate count and a count histogram

@@ -406,6 +406,18 @@ extern "C" int scone_discover_fgrams(const int32_t* token_ids, int64_t B, int64_
     if (workspace && (workspace_bytes < 0 || (uint64_t)workspace_bytes < lay.total))
         return SCONE_EINVAL;
     if ((uintptr_t)workspace % 256 != 0) return SCONE_EINVAL;
+    // The selection writes the outputs while it reads candidates from the
+    // workspace, and the scans read the corpus while they write the
+    // workspace: no two of these buffers may share memory.
+    {
+        const void* buf[5] = {token_ids, fgrams, lengths, counts, workspace};
+        const int64_t len[5] = {span_bytes(BT, 4), span_bytes(S, 4 * (int64_t)max_len),
+                                span_bytes(S, 4), span_bytes(S, 4),
+                                workspace ? (int64_t)lay.total : 0};
+        for (int i = 0; i < 5; ++i)
+            for (int j = i + 1; j < 5; ++j)
+                if (overlaps(buf[i], len[i], buf[j], len[j])) return SCONE_EINVAL;
+    }
     hipStream_t st = static_cast<hipStream_t>(stream);
 
     const uint64_t cap = lay.cap;

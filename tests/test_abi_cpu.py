@@ -256,3 +256,29 @@ def test_split_gather_rejects_workspace_and_count_aliasing():
         assert G(ids, n, near, nn, far, nf, R, out, ws, need, c, None) == E
         assert F(ids, n, near, nn, far, nf, R, out, c, None) == E
     assert F(ids, n, near, nn, far, nf, R, out, cnt, None) == H
+
+
+def test_discovery_rejects_shared_buffers():
+    """No two of the corpus, the three outputs and the workspace may share
+    memory; a call whose buffers are apart gets past the checks and only
+    then fails here, at its first HIP call."""
+    L = S.scone.lib()
+    E, H = S.scone.EINVAL, S.scone.EHIP
+    D = L.scone_discover_fgrams
+    B, T, K, Sn = 4, 1000, 3, 500
+    tok, fg, ln, cnt, ws = (_fake(k << 32) for k in (1, 2, 3, 4, 5))
+    need = L.scone_discover_workspace(B, T, K)
+    assert need > 0
+    nf = ctypes.c_int64(-1)
+    assert D(tok, B, T, K, 5, Sn, fg, ln, cnt, ctypes.byref(nf), ws, need, None) == H
+    assert nf.value == 0
+    assert D(tok, B, T, K, 5, Sn, fg, _fake((1 << 32) + 4 * B * T - 4), cnt, ctypes.byref(nf),
+             ws, need, None) == E                                      # lengths ends in corpus
+    assert D(tok, B, T, K, 5, Sn, _fake((3 << 32) - 4 * Sn * K + 4), ln, cnt, ctypes.byref(nf),
+             ws, need, None) == E                                      # fgrams runs into lengths
+    assert D(tok, B, T, K, 5, Sn, fg, ln, _fake((3 << 32) + 4 * Sn - 4), ctypes.byref(nf),
+             ws, need, None) == E                                      # counts over lengths
+    assert D(tok, B, T, K, 5, Sn, fg, ln, cnt, ctypes.byref(nf), _fake((2 << 32) + 256), need,
+             None) == E                                                # workspace in fgrams
+    assert D(tok, B, T, K, 5, Sn, fg, ln, cnt, ctypes.byref(nf),
+             _fake(((1 << 32) - need + 512) // 256 * 256), need, None) == E  # into corpus
