@@ -1222,8 +1222,7 @@ def reduce_trace(trace_csv, plan_path, bench_json, out_md, profile_cmd, bench_pl
     med = lambda L: st.median(x["ns"] for x in L) / 1e3
     span = lambda L: f"{L[0]['Dispatch_Id']}-{L[-1]['Dispatch_Id']}"
     cfgname = plan["config"]
-    srcs = sorted({s for v in KERNEL_SOURCES.values() for s in v}
-                  | {"lookup.hip", "decode.hip", "gather_split.hip", "runtime.hip"})
+    srcs = kernel_sources(set(by))
     L = [f"# Kernel trace: {cfgname} ({plan['workload']})\n",
          "Command (one MI355X, `<repo>` the repository root):\n", f"    {profile_cmd}\n",
          "Reduced with `python bench.py --reduce-trace <out>/run_kernel_trace.csv "
