@@ -21,12 +21,15 @@
 // four accumulators are four consecutive n of one row m: the epilogue writes
 // 8 bytes (bf16) or 16 bytes (f32) per lane per tile.
 //
-// Bias-only products (kBias) stage the finished bf16 tile in LDS after the
+// The bf16 epilogues (kBias, kGelu) stage the finished tile in LDS after the
 // last slab and store it row by row: a lane's accumulators hold 4 consecutive
 // n of one row m, so written straight from registers a row gets 32 bytes per
 // store instruction; through LDS each store instruction writes whole 256-byte
-// row segments (measured 6-15% faster on the q/k/v product, no faster with the
-// GELU or residual epilogues, which keep the direct stores).
+// row segments.  Those stores are non-temporal: the outputs (hundreds of MB)
+// are read back by the next kernel, never by this one, and streaming them past
+// the caches made the q/k/v and fc1 products 6-7% faster at M = 65,536 (the
+// narrow direct stores lose with the same hint).  The residual epilogue reads
+// its output first and keeps the direct stores.
 //
 // LDS layout: a slab row is 64 elements = 128 bytes = eight 16-byte chunks,
 // stored at slot chunk ^ (row & 7).  A fragment read touches 16 consecutive
@@ -120,7 +123,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
     constexpr int STAGE = (BM + BN) * kRowBytes;
     constexpr int GA = BM / 8 / NW, GW = BN / 8 / NW;  // 8-row copy groups per wavefront
     static_assert(GA * 8 * NW == BM && GW * 8 * NW == BN, "copy groups must split evenly");
-    static_assert(!kStaged || EPI == kBias, "only the bias epilogue is staged");
+    static_assert(!kStaged || EPI != kResid, "the residual epilogue is not staged");
     constexpr int ERS = WTN * 2 + 16;  // staged row stride: 16 bytes of padding per row
     constexpr int SMEM = kStaged && NW * WTM * ERS > 2 * STAGE ? NW * WTM * ERS : 2 * STAGE;
     __shared__ __attribute__((aligned(1024))) uint8_t smem[SMEM];
@@ -296,9 +299,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
             const float b2 = bf16_to_f32(bb[i].y & 0xFFFFu), b3 = bf16_to_f32(bb[i].y >> 16);
 #pragma unroll
             for (int j = 0; j < TM; ++j) {
+                float v0 = acc[i][j][0] + b0, v1 = acc[i][j][1] + b1;
+                float v2 = acc[i][j][2] + b2, v3 = acc[i][j][3] + b3;
+                if (EPI == kGelu) {
+                    v0 = gelu_erf(v0); v1 = gelu_erf(v1); v2 = gelu_erf(v2); v3 = gelu_erf(v3);
+                }
                 u32x2 o;
-                o.x = pack_bf16x2(acc[i][j][0] + b0, acc[i][j][1] + b1);
-                o.y = pack_bf16x2(acc[i][j][2] + b2, acc[i][j][3] + b3);
+                o.x = pack_bf16x2(v0, v1);
+                o.y = pack_bf16x2(v2, v3);
                 *reinterpret_cast<u32x2*>(wb + (j * 16 + (elane & 15)) * ERS +
                                           (i * 16 + (elane >> 4) * 4) * 2) = o;
             }
@@ -314,7 +322,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
             const int m = m0 + wm * WTM + r;
             const u32x4 v = *reinterpret_cast<const u32x4*>(wb + r * ERS + cc * 16);
             if (m < M)
-                *reinterpret_cast<u32x4*>(ob + (int64_t)m * ldc + n0 + wn * WTN + cc * 8) = v;
+                __builtin_nontemporal_store(
+                    v, reinterpret_cast<u32x4*>(ob + (int64_t)m * ldc + n0 + wn * WTN + cc * 8));
         }
         return;
     }
@@ -380,8 +389,8 @@ inline hipError_t launch_tiles(const uint16_t* A, const uint16_t* W, const uint1
     const int tiles_m = (M + BM - 1) / BM;
     const dim3 grid((unsigned)(tiles_m * tiles_n)), block(64 * WGM * WGN);
     // The staged store writes 16-byte pieces: rows must start 16-byte aligned.
-    if (EPI == kBias && ldc % 8 == 0 && (uintptr_t)out % 16 == 0)
-        hipLaunchKernelGGL((k_gemm<EPI, BM, BN, WGM, WGN, EPI == kBias>), grid, block, 0, st, A,
+    if (EPI != kResid && ldc % 8 == 0 && (uintptr_t)out % 16 == 0)
+        hipLaunchKernelGGL((k_gemm<EPI, BM, BN, WGM, WGN, EPI != kResid>), grid, block, 0, st, A,
                            W, bias, out, ldc, M, N, K, tiles_n);
     else
         hipLaunchKernelGGL((k_gemm<EPI, BM, BN, WGM, WGN, false>), grid, block, 0, st, A, W,
