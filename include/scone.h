@@ -391,7 +391,8 @@ int64_t scone_discover_workspace(int64_t B, int64_t T, int32_t max_len);
  *  d         d_model, a multiple of 512 up to 4096; d / n_heads must be 64 or
  *            128; d_ff a multiple of 128; n_layers >= 0 (0 gives
  *            LNf(T(w_{n-1}) + pos[n-1])).
- *  rows      [n_rows, d] bf16 output table (device memory).
+ *  rows      [n_rows, d] bf16 output table (device memory); sharing memory
+ *            with fgrams, lengths, row_ids or params gives SCONE_EINVAL.
  *
  * tok_rows, params and rows must be 16-byte aligned (else SCONE_EINVAL).
  * Synchronous: returns after the rows are written, with the first data error

@@ -487,6 +487,19 @@ extern "C" int scone_fgram_model_forward(const int32_t* fgrams, const int32_t* l
     if (!fgrams || !lengths || !row_ids || !tok_rows || !params || !rows) return SCONE_EINVAL;
     if (((uintptr_t)tok_rows | (uintptr_t)params | (uintptr_t)rows) % 16 != 0)
         return SCONE_EINVAL;
+    // Rows are written chunk by chunk while later chunks still read the
+    // f-grams, lengths, row ids and parameters: `rows` may share memory with
+    // none of them (tok_rows may lie inside it, as documented).
+    {
+        int64_t p_elems = 0;
+        for (int64_t e : param_sizes(d, d_ff, n_layers, max_len)) p_elems += align_up(e);
+        const int64_t rb = span_bytes(n_rows, 2 * (int64_t)d);
+        if (overlaps(rows, rb, fgrams, span_bytes(n, 4 * (int64_t)max_len)) ||
+            overlaps(rows, rb, lengths, span_bytes(n, 4)) ||
+            overlaps(rows, rb, row_ids, span_bytes(n, 4)) ||
+            overlaps(rows, rb, params, span_bytes(p_elems, 2)))
+            return SCONE_EINVAL;
+    }
     hipStream_t st = static_cast<hipStream_t>(stream);
     const ChunkFn fn = chunk_fn(d);
     if (!fn) return SCONE_EINVAL;

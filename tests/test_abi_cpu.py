@@ -282,3 +282,28 @@ def test_discovery_rejects_shared_buffers():
              None) == E                                                # workspace in fgrams
     assert D(tok, B, T, K, 5, Sn, fg, ln, cnt, ctypes.byref(nf),
              _fake(((1 << 32) - need + 512) // 256 * 256), need, None) == E  # into corpus
+
+
+def test_fgram_model_rejects_rows_over_its_inputs():
+    """The output table may not share memory with the f-grams, lengths, row
+    ids or parameters (the token rows may lie inside it); a call whose
+    buffers are apart gets past the checks and only then fails here, at its
+    first allocation."""
+    L = S.scone.lib()
+    E = S.scone.EINVAL
+    Fw = L.scone_fgram_model_forward
+    n, K, V, d, heads, dff, layers, n_rows = 100, 3, 50, 512, 8, 1024, 1, 200
+    total = ctypes.c_int64()
+    assert L.scone_fgram_model_layout(d, heads, dff, layers, K, None, None,
+                                      ctypes.byref(total)) == S.scone.OK
+    fg, ln, ids, prm, rows = (_fake(k << 32) for k in (1, 2, 3, 4, 5))
+    tok = _fake((5 << 32))                       # the unified table: T inside rows
+    rb = n_rows * d * 2
+
+    def call(fg=fg, ln=ln, ids=ids, prm=prm, rows=rows):
+        return Fw(fg, ln, ids, n, K, tok, V, prm, d, heads, dff, layers, rows, n_rows, None)
+    assert call() not in (E, S.scone.OK)         # past the checks: fails allocating
+    assert call(rows=_fake((1 << 32) - rb + 16)) == E           # rows end in the f-grams
+    assert call(ln=_fake((5 << 32) + rb - 4)) == E              # lengths at the table's end
+    assert call(ids=_fake((5 << 32) + 1024)) == E               # row ids inside the table
+    assert call(prm=_fake((5 << 32) - 2 * total.value + 16)) == E  # params run into it
