@@ -7,7 +7,12 @@ from workloads import fill_table, torch_dtype
 
 
 def dev(a, device="cuda"):
-    return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+    a = np.ascontiguousarray(a)
+    # a reversed axis of length 1 keeps its negative stride through
+    # ascontiguousarray (the array still counts as contiguous); torch refuses it
+    if any(s < 0 for s in a.strides):
+        a = a.copy()
+    return torch.from_numpy(a).to(device)
 
 
 def build_gpu(fgrams, lengths, ids, max_load=0.5):
