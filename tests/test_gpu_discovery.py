@@ -5,6 +5,8 @@ arbitrarily), so a result is checked for what is unique: its size, that every
 f-gram is a real candidate with the oracle's count, and that no candidate
 counting more than the smallest kept count was left out.
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -142,3 +144,23 @@ def test_workspace_paths_agree():
         check_top_s(fg, ln, ct, cands, Sn)
     assert call(ws.data_ptr(), need - 1)[0] == S.scone.EINVAL
     assert call(ws.data_ptr() + 16, need)[0] == S.scone.EINVAL
+
+
+# Random corpora (seeds 70000 + case): vocabularies of 2 to 30,000, K 2-7,
+# minimum counts 1-5, three values of S each.  SCONE_DISCOVERY_SWEEP sets the
+# number of cases (1,000 take under a minute).
+DISC_CASES = int(os.environ.get("SCONE_DISCOVERY_SWEEP", "20"))
+
+
+@pytest.mark.parametrize("case", range(DISC_CASES))
+def test_random_corpora(case):
+    rng = np.random.default_rng(70000 + case)
+    V = int(rng.choice([2, 3, 7, 50, 1000, 30000]))
+    K = int(rng.integers(2, 8))
+    mc = int(rng.integers(1, 6))
+    B, T = int(rng.integers(1, 9)), int(rng.integers(1, 2500))
+    X = rng.integers(0, V, size=(B, T)).astype(np.int32)
+    cands = discovery.candidates(X, K, mc)
+    for Sn in (1, int(rng.integers(2, 300)), 10 ** 6):
+        fg, ln, ct = S.discover_fgrams(dev(X), K, Sn, mc)
+        check_top_s(fg, ln, ct, cands, Sn)

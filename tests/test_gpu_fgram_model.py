@@ -16,6 +16,8 @@ within 12 eps(L) times its row's rms.  A dropped bias or gain (0.1 relative
 with the "unit" parameters), a wrong mask, position or head split moves rows
 by far more.
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -268,3 +270,33 @@ def test_full_size_gpt2_128m_on_1m_fgrams():
                       {k: bf16_bits_to_f64(v) for k, v in P.items()}, cfg.n_layers, cfg.n_heads)
     got = as_f64(rows[torch.from_numpy(w.ids[sample].astype(np.int64)).cuda()])
     assert_close(got, ref, cfg.n_layers, "sampled rows")
+
+
+# Random model shapes (seeds 50000 + case): widths that are not multiples of
+# 256, fc2 depths down to two 64-deep slabs, 0-2 layers, 1 to 5,000 f-grams.
+# SCONE_MODEL_SWEEP sets the number of cases (1,000 take about four minutes).
+MODEL_CASES = int(os.environ.get("SCONE_MODEL_SWEEP", "6"))
+
+
+@pytest.mark.parametrize("case", range(MODEL_CASES))
+def test_random_model_shapes(case):
+    rng = np.random.default_rng(50000 + case)
+    d = int(rng.choice([512, 1024, 1536, 2048]))
+    dh = int(rng.choice([64, 128]))
+    d_ff = int(rng.choice([128, 384, 512, 1024, 2048, 4096]))
+    layers = int(rng.integers(0, 3))
+    K = int(rng.integers(2, 8))
+    N = int(rng.choice([1, 2, 7, 15, 16, 17, 255, 256, 257, 1000, 3000,
+                        int(rng.integers(1, 5000))]))
+    V = int(rng.choice([5, 300, 5000]))
+    cfg = ModelConfig(d, d // dh, d_ff, layers, K)
+    P = make_params(cfg, seed=case)
+    T = make_token_rows(V, d, seed=case + 1)
+    fg, lengths = random_fgrams(rng, V, N, K)
+    row_ids = (rng.permutation(N) + 3).astype(np.int32)
+    got = as_f64(run(cfg, fg, lengths, row_ids, T, P, N + 3))
+    sample = np.sort(rng.choice(N, min(N, 200), replace=False))
+    ref = orc.forward(fg[sample], lengths[sample], bf16_bits_to_f64(T),
+                      {k: bf16_bits_to_f64(v) for k, v in P.items()}, layers, d // dh)
+    assert_close(got[row_ids[sample]], ref, layers, f"case {case}")
+    assert not got[[0, 1, 2]].any()

@@ -9,6 +9,8 @@ fused kernel byte for byte, a two-batch pipelined stream, decoding step by step
 against prefill, and the split placement.  The sweep is deterministic (fixed seeds) and prints the case
 it is on.
 """
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -50,7 +52,12 @@ def draw_case(rng):
     return K, V, X, fg, lengths, ids, max_n, row_bytes, max_load
 
 
-@pytest.mark.parametrize("block", range(4))
+# Blocks of 15 cases (seeds 9000 + case); SCONE_SWEEP_BLOCKS widens the sweep
+# (700 blocks = 10,500 cases, about eight minutes on one MI355X).
+BLOCKS = int(os.environ.get("SCONE_SWEEP_BLOCKS", "4"))
+
+
+@pytest.mark.parametrize("block", range(BLOCKS))
 def test_random_sweep(block):
     for case in range(block * 15, block * 15 + 15):
         rng = np.random.default_rng(9000 + case)
