@@ -15,7 +15,9 @@
 // buffered in registers: a slab is two 32-deep halves, and the LDS reads of
 // one half are in flight while the matrix cores multiply the other, so the
 // products of a slab's second half run after the barrier while the next
-// slab's first fragments load.  Each wavefront owns a
+// slab's first fragments load.  The reads and copies are slotted one after
+// each product (see `step` below) rather than issued as a block.  Each
+// wavefront owns a
 // (BM / WGM) x (BN / WGN) part of the tile as 16 x 16 v_mfma_f32_16x16x32_bf16
 // tiles.  W is the instruction's first operand and A the second, so a lane's
 // four accumulators are four consecutive n of one row m: the epilogue writes
