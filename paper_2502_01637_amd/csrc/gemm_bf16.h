@@ -131,13 +131,23 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const uint16_t* __restr
     __shared__ __attribute__((aligned(1024))) uint8_t smem[SMEM];
 
     // Consecutive workgroups land on different XCDs; renumber so that each
-    // XCD walks a contiguous run of tiles (n fastest), which keeps the A rows
-    // of a tile row in that XCD's L2 while its n-tiles are computed.
+    // XCD walks a contiguous run of tiles, and order that run in groups of
+    // kGroupM tile rows, m fastest inside a group, so that the workgroups an
+    // XCD runs at once share A and W slabs in its L2: 32 of them as 8 rows by
+    // 4 columns touch 12 slabs per k-step, where a run along n touches 15 on
+    // a 12-column product and 18 on a 16-column one (4-column products were
+    // 8 by 4 already).
+    constexpr int kGroupM = 8;
     const int nb = gridDim.x;
     const int b = blockIdx.x;
     const int per = nb / 8;
     const int t = (b < per * 8) ? (b % 8) * per + b / 8 : b;
-    const int tm = t / tiles_n, tn = t % tiles_n;
+    const int tiles_m = (M + BM - 1) / BM;
+    const int group = t / (kGroupM * tiles_n);
+    const int first = group * kGroupM;
+    const int gm = tiles_m - first < kGroupM ? tiles_m - first : kGroupM;
+    const int tr = t - group * kGroupM * tiles_n;
+    const int tm = first + tr % gm, tn = tr / gm;
     const int m0 = tm * BM, n0 = tn * BN;
 
     const int lane = threadIdx.x & 63;
