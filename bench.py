@@ -709,10 +709,17 @@ def run_prefill(args, cfg):
     ml = ml0.cpu().numpy()
     result["match"] = match_stats(ml, cfg.max_n)
     result["build_ms"] = build_s * 1e3
+    host_pp = probes_per_position(cfg, w, batches_np[0])
+    _, _, dev_probes = S.lookup_counted(table, X[0], cfg.max_n)
+    PLAN.add("probe_count", "k_lookup", 1)
     result["probes"] = {
-        "per_position_kernel_schedule": probes_per_position(cfg, w, batches_np[0]),
+        "per_position_kernel_schedule": host_pp,
         "counted": "on the host, replaying the tile lookup's pruned two-lane schedule over "
                    "batch 0 (each probe reads one 64-byte bucket, more only when it is full)",
+        "per_position_device": dev_probes / cfg.n_tok,
+        "device_counted": "on the device: scone_lookup_counted over batch 0 (the same kernel "
+                          "instantiated with a probe counter)",
+        "device_equals_host_replay": dev_probes == round(host_pp * cfg.n_tok),
         "max_per_position": max(cfg.max_n - 1, 0)}
 
     if not args.no_cpu_baseline:

@@ -127,6 +127,22 @@ int scone_lookup(const scone_table_t* table, const int32_t* token_ids, int64_t B
                  void* stream);
 
 /*
+ * scone_lookup that also counts its hash probes (Section 4.3 reports up to
+ * four queries per token for K = 5; this measures how many the kernel makes):
+ * *probes, a device uint64, is increased by the number of keys probed, one
+ * per tested length of every position.  Lengths 2 and 3 are tested at every
+ * position where they fit the window; 4 and 5 only where the length-3 suffix
+ * ends some f-gram of length 4 or more, and 6 and 7 where, in addition, the
+ * length-5 suffix ends one of length 6 or more.  Arguments, results and errors
+ * are those of scone_lookup; probes may not be NULL (SCONE_EINVAL) or share
+ * memory with the other buffers (SCONE_EINVAL).  The count is a diagnostic:
+ * the same kernel built with a counter, for tests and measurements.
+ */
+int scone_lookup_counted(const scone_table_t* table, const int32_t* token_ids, int64_t B,
+                         int64_t T, int32_t max_n, int32_t* fgram_ids, int8_t* match_len,
+                         uint64_t* probes, void* stream);
+
+/*
  * Pre-scan tagging (the paper tags every training token with the length of
  * its longest matching f-gram before training, implementation details in the
  * appendix; the mean of these lengths is the average match length that

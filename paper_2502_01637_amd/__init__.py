@@ -6,7 +6,8 @@ precompute of the f-gram rows as HIP kernels; ``scone`` is its
 Python binding.
 """
 from . import scone
-from .scone import (SconeError, Table, HostRows, build_fgram_table, lookup, gather, embed,
+from .scone import (SconeError, Table, HostRows, build_fgram_table, lookup, lookup_counted,
+                    gather, embed,
                     embed_pipelined,
                     decode_step, gather_split, split_workspace_bytes, tag, discover_fgrams,
                     discover_workspace_bytes,

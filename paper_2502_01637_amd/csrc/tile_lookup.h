@@ -46,12 +46,15 @@ __device__ __forceinline__ void stage_tokens(int32_t* s_tok, const int32_t* __re
 // standalone lookup by about a fifth.  Returns, on lane j = 0 of a valid
 // position (p < P, t0 + p < T), the id (or the token itself) and the matched
 // length (1 when nothing matched); `tok_ok` reports whether the position's
-// own token is in range.  All lanes of the wave must call it.
-template <int SB, int G>
+// own token is in range.  All lanes of the wave must call it.  With kCount,
+// the wave also adds the number of keys it probed to *probes (a diagnostic
+// instantiation; the lookup itself is the same).
+template <int SB, int G, bool kCount = false>
 __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __restrict__ slots,
                                             uint64_t mask, const int32_t* s_tok, int64_t T,
                                             int64_t t0, int P, int max_n, int32_t& id_out,
-                                            int& len_out, bool& tok_ok) {
+                                            int& len_out, bool& tok_ok,
+                                            unsigned long long* probes = nullptr) {
     static_assert(G == 1 || G == 2, "one or two lanes per position");
     const int halo = max_n - 1;
     const int p = threadIdx.x / G;
@@ -64,6 +67,7 @@ __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __
     int best = 0;  // longest f-gram length this lane found
     int32_t best_id = 0;
     bool ext = false;  // the last probed key has an entry with kExtBit
+    int n_probes = 0;  // keys this lane probed (kCount)
     auto step = [&](int n) {
         ext = false;
         if (!(valid && n >= 2 && n <= max_n && (int64_t)n <= t + 1)) return;
@@ -73,6 +77,7 @@ __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __
         for (int i = 0; i < SCONE_MAX_FGRAM_LEN; ++i)
             if (i < n) ok &= (win[i] >= 0) & (win[i] < SCONE_TOKEN_LIMIT);
         int32_t raw = 0;
+        if constexpr (kCount) n_probes += ok ? 1 : 0;
         if (ok && probe_raw<SB>(slots, mask, pack_key(win, n), raw)) {
             if (entry_is_fgram(raw)) {
                 best = n;
@@ -101,6 +106,12 @@ __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __
     }
     id_out = best ? best_id : tok;
     len_out = best ? best : 1;
+    if constexpr (kCount) {
+#pragma unroll
+        for (int w = 32; w >= 1; w >>= 1) n_probes += __shfl_xor(n_probes, w);
+        if ((threadIdx.x & 63) == 0 && n_probes)
+            atomicAdd(probes, (unsigned long long)n_probes);
+    }
 }
 
 // One workgroup's share of a lookup over X [B, T]: tile `tile` of the row-major
@@ -109,14 +120,15 @@ __device__ __forceinline__ void tile_lookup(const typename SlotOps<SB>::Slot* __
 // length (either output may be null); a bad token raises SCONE_ETOKEN.
 // Returns the matched length on the lane that wrote a position, else 0.
 // Called by the whole workgroup (it synchronises once).
-template <int SB, int G>
+template <int SB, int G, bool kCount = false>
 __device__ __forceinline__ int lookup_block(const typename SlotOps<SB>::Slot* __restrict__ slots,
                                             uint64_t mask, const int32_t* __restrict__ X,
                                             int64_t T, int max_n, int64_t tiles_per_row,
                                             int64_t tile, int32_t* s_tok,
                                             int32_t* __restrict__ ids_out,
                                             int8_t* __restrict__ len_out,
-                                            unsigned* __restrict__ err) {
+                                            unsigned* __restrict__ err,
+                                            unsigned long long* probes = nullptr) {
     constexpr int P = TileShape<G>::kPositions;
     const int64_t b = tile / tiles_per_row;
     const int64_t t0 = (tile - b * tiles_per_row) * (int64_t)P;
@@ -125,7 +137,7 @@ __device__ __forceinline__ int lookup_block(const typename SlotOps<SB>::Slot* __
     int32_t id;
     int len;
     bool tok_ok;
-    tile_lookup<SB, G>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok);
+    tile_lookup<SB, G, kCount>(slots, mask, s_tok, T, t0, P, max_n, id, len, tok_ok, probes);
     const int64_t t = t0 + threadIdx.x / G;
     if (threadIdx.x % G == 0 && t < T) {
         if (!tok_ok) atomicOr(err, err_bit(SCONE_ETOKEN));

@@ -42,6 +42,8 @@ def _declare(L):
     L.scone_build_fgram_table.restype = I
     L.scone_lookup.argtypes = [P, P, I64, I64, I32, P, P, P]
     L.scone_lookup.restype = I
+    L.scone_lookup_counted.argtypes = [P, P, I64, I64, I32, P, P, P, P]
+    L.scone_lookup_counted.restype = I
     L.scone_gather.argtypes = [P, I64, P, I64, I64, P, I32, P]
     L.scone_gather.restype = I
     L.scone_embed.argtypes = [P, P, I64, I64, I32, P, I64, I64, I32, P, P, P, P]
@@ -200,6 +202,23 @@ def lookup(table: Table, token_ids: torch.Tensor, max_n: int,
                                 _ptr(fgram_ids), _ptr(match_len), _stream(stream))
     _check(rc, "scone_lookup")
     return fgram_ids, match_len
+
+
+def lookup_counted(table: Table, token_ids: torch.Tensor, max_n: int,
+                   stream=None) -> Tuple[torch.Tensor, torch.Tensor, int]:
+    """scone_lookup_counted on token_ids [B, T]: (fgram_ids, match_len, keys
+    probed).  Synchronises the stream to read the count."""
+    _dev_i32(token_ids, "token_ids", 2)
+    B, T = token_ids.shape
+    fgram_ids = torch.empty((B, T), dtype=torch.int32, device=token_ids.device)
+    match_len = torch.empty((B, T), dtype=torch.int8, device=token_ids.device)
+    probes = torch.zeros(1, dtype=torch.int64, device=token_ids.device)
+    with torch.cuda.device(token_ids.device):
+        rc = lib().scone_lookup_counted(table.handle, _ptr(token_ids), B, T, int(max_n),
+                                        _ptr(fgram_ids), _ptr(match_len), _ptr(probes),
+                                        _stream(stream))
+    _check(rc, "scone_lookup_counted")
+    return fgram_ids, match_len, int(probes.item())
 
 
 def tag(table: Table, token_ids: torch.Tensor, max_n: int,

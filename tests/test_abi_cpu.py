@@ -307,3 +307,25 @@ def test_fgram_model_rejects_rows_over_its_inputs():
     assert call(ln=_fake((5 << 32) + rb - 4)) == E              # lengths at the table's end
     assert call(ids=_fake((5 << 32) + 1024)) == E               # row ids inside the table
     assert call(prm=_fake((5 << 32) - 2 * total.value + 16)) == E  # params run into it
+
+
+def test_counted_lookup_host_checks():
+    """scone_lookup_counted needs its counter, and the counter may not share
+    memory with the tokens or the outputs; otherwise it checks like
+    scone_lookup and gets as far as its first HIP call."""
+    L = S.scone.lib()
+    E, H = S.scone.EINVAL, S.scone.EHIP
+    C = L.scone_lookup_counted
+    tbl = ctypes.create_string_buffer(64)
+    B, T = 4, 256
+    n = B * T
+    tok, ids, ln, cnt = _fake(1 << 32), _fake(2 << 32), _fake(3 << 32), _fake(4 << 32)
+    assert C(tbl, tok, B, T, 3, ids, ln, None, None) == E                 # no counter
+    assert C(None, tok, B, T, 3, ids, ln, cnt, None) == E                 # no table
+    assert C(tbl, tok, B, T, 0, ids, ln, cnt, None) == E                  # max_n < 1
+    assert C(tbl, tok, B, T, 3, ids, ln, _fake((1 << 32) + 4 * n - 8), None) == E  # in tokens
+    assert C(tbl, tok, B, T, 3, ids, ln, _fake((2 << 32) + 64), None) == E         # in ids
+    assert C(tbl, tok, B, T, 3, ids, ln, _fake((3 << 32) + n - 1), None) == E      # in lengths
+    assert C(tbl, tok, B, T, 3, _fake((1 << 32) + 4), ln, cnt, None) == E          # ids over tokens
+    assert C(tbl, tok, B, T, 3, ids, ln, cnt, None) == H
+    assert C(tbl, tok, 0, T, 3, ids, ln, cnt, None) == S.scone.OK

@@ -134,3 +134,61 @@ def test_dense_tables_all_paths(max_len, V, n):
         got[:, t] = fid.cpu().numpy()
     S.check_ok()
     np.testing.assert_array_equal(got, exp_ids)
+
+
+def literal_probe_count(fgrams, X, max_n, max_len):
+    """Keys the tile lookup probes, walked position by position from its rule:
+    with a window of w = min(max_n, K, t + 1) tokens, lengths 2 and 3 where
+    they fit (only 2 when the window is capped at 2); 4 and 5 where they fit
+    and the length-3 suffix ends some f-gram of length 4 or more; 6 and 7
+    where, in addition, the length-5 suffix (which must fit) ends one of
+    length 6 or more."""
+    ends = {3: set(), 5: set()}
+    for g in fgrams:
+        for n in (3, 5):
+            if len(g) >= n + 1:
+                ends[n].add(tuple(g[-n:]))
+    cap = min(max_n, max_len)
+    total = 0
+    for row in np.asarray(X):
+        for t in range(len(row)):
+            w = min(cap, t + 1)
+            if cap <= 2:
+                total += int(w >= 2)
+                continue
+            total += int(w >= 2) + int(w >= 3)
+            go4 = w >= 3 and tuple(row[t - 2:t + 1]) in ends[3]
+            if go4:
+                total += int(w >= 4) + int(w >= 5)
+                if cap >= 6 and w >= 5 and tuple(row[t - 4:t + 1]) in ends[5]:
+                    total += int(w >= 6) + int(w >= 7)
+    return total
+
+
+@pytest.mark.parametrize("max_len,V,n", [(5, 6, 300), (7, 4, 400), (3, 5, 100), (5, 40, 2000)])
+def test_device_probe_count_matches_the_schedule(max_len, V, n):
+    """scone_lookup_counted's device count equals the literal walk of the
+    pruned schedule, and its ids and lengths equal scone_lookup's."""
+    rng = np.random.default_rng(max_len * 100 + V)
+    X = rng.integers(0, V, size=(3, 257)).astype(np.int32)
+    fgrams, seen = [], set()
+    while len(fgrams) < n:
+        L = int(rng.integers(2, max_len + 1))
+        if rng.random() < 0.5:                      # windows of X, so every length hits
+            b, t = int(rng.integers(3)), int(rng.integers(L - 1, X.shape[1]))
+            g = tuple(int(v) for v in X[b, t - L + 1:t + 1])
+        else:
+            g = tuple(int(v) for v in rng.integers(0, V, size=L))
+        if g not in seen:
+            seen.add(g)
+            fgrams.append(list(g))
+    ids = list(range(1000, 1000 + len(fgrams)))
+    fg = pad(fgrams, max_len)
+    tb = build_gpu(fg, [len(g) for g in fgrams], ids)
+    Xd = dev(X)
+    for max_n in sorted({2, 3, max_len, max_len + 2}):
+        want_ids, want_len = S.lookup(tb, Xd, max_n, want_len=True)
+        got_ids, got_len, probes = S.lookup_counted(tb, Xd, max_n)
+        S.check_ok()
+        assert torch.equal(got_ids, want_ids) and torch.equal(got_len, want_len), max_n
+        assert probes == literal_probe_count(fgrams, X, max_n, max_len), max_n
