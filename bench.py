@@ -268,7 +268,7 @@ def probes_per_position(cfg, w, X: np.ndarray) -> float:
         return win.reshape(B * T, n).view(np.dtype((np.void, 4 * n))).reshape(B, T)
 
     def flagged(n):
-        """Positions whose length-n suffix ends an f-gram longer than n + 1."""
+        """Positions whose length-n suffix ends an f-gram of length n + 1 or more."""
         long_ = w.lengths >= n + 1
         if not long_.any():
             return np.zeros((B, T), dtype=bool)
